@@ -1,0 +1,210 @@
+"""Benchmark of the SegPagedAttention hot path on one MI355X.
+
+A step is one pass of the hot path over one batch of synthetic input: page
+selection (seg_paged_attn_select) and the attention forward with its split
+combine (seg_paged_attn_fwd). The default workload is the Llama-3-8B-shaped
+sparse decode: 16 requests, 32 query / 8 KV heads, head dim 128, 32K context
+in 2048-token segments, page 16, 25% of the pages of every KV head selected
+(first and last segment included).
+
+Output: one JSON line. `value` is attended KV tokens per second for the whole
+step (inputs resident in HBM). `roofline` is the dominant kernel
+(decode_attn): algorithmic bytes per launch over its mean launch time,
+measured with HIP events on the launch stream. `cpu_baseline` is the fp64
+oracle timed on this host's cores on a sample of the same step.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "attended KV tokens/s and achieved HBM GB/s (% of peak) for sparse decode"
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def algorithmic_bytes(wl, sel_indptr, sel_pages):
+    """Bytes the attention launch must move: selected valid K and V, Q, O,
+    and the index reads (page id, page-table entry) of every selected page."""
+    tokens = wl.attended_tokens(sel_indptr, sel_pages)
+    kv = tokens * 2 * wl.D * 2
+    rows = wl.total_q * wl.Hq
+    qo = rows * wl.D * 2 * 2
+    idx = int(sel_indptr[-1]) * 8
+    return tokens, kv + qo + idx
+
+
+def attention_flops(wl, sel_indptr, sel_pages):
+    """2 * 2 * D flops per visible (query row, key) pair (QK^T and PV)."""
+    tot = 0
+    P = wl.P
+    for u in range(wl.num_units):
+        r = u // wl.Hkv
+        L = int(wl.ctx_lens[r])
+        nq = int(wl.q_indptr[r + 1] - wl.q_indptr[r])
+        pg = sel_pages[sel_indptr[u]:sel_indptr[u + 1]].astype(np.int64)
+        tok = (pg[:, None] * P + np.arange(P)[None, :]).reshape(-1)
+        tok = tok[tok < L]
+        for i in range(nq):
+            tot += int(np.sum(tok <= L - nq + i)) * wl.G
+    return 4 * wl.D * tot
+
+
+def cpu_baseline(wl, min_seconds=10.0, max_seconds=30.0):
+    """fp64 oracle (select + attention) on a sample of the step's units."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import segpa_oracle as O
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    U = wl.num_units
+    n_sample = min(U, 32)
+    step = max(1, U // n_sample)
+    units = list(range(0, U, step))[:n_sample]
+    q64 = wl.q("cpu").double().numpy()
+    kv = {u: wl.unit_kv(*divmod(u, wl.Hkv), "cpu") for u in units}   # bf16, not timed
+    sp = wl.spec
+    tokens = 0
+    passes = 0
+    t0 = time.perf_counter()
+    with threadpool_limits(limits=1):
+        while True:
+            for u in units:
+                r, g = divmod(u, wl.Hkv)
+                K = kv[u][0].double().numpy()
+                V = kv[u][1].double().numpy()
+                sel = O.select(sp.sel_mode, wl.ctx_lens, wl.q_indptr, wl.Hq, wl.Hkv, wl.P,
+                               budgets=wl.budgets, forced_head=sp.forced_head,
+                               forced_tail=sp.forced_tail, seed=sp.sel_seed,
+                               head_policy=wl.head_policy, n_sink=sp.n_sink, window=sp.window,
+                               q=q64, kv_of_unit=lambda rr, gg: (K, V), units=[u])[u]
+                O.forward_unit(q64, wl.q_indptr, wl.ctx_lens, wl.Hq, wl.Hkv, wl.P, u, sel, K, V)
+                L = int(wl.ctx_lens[r])
+                tokens += int(sum(min(wl.P, L - p * wl.P) for p in sel))
+                if time.perf_counter() - t0 > max_seconds:
+                    break
+            passes += 1
+            el = time.perf_counter() - t0
+            if el >= min_seconds or el > max_seconds:
+                break
+    el = time.perf_counter() - t0
+    return {"value": tokens / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{len(units)} of {U} (request, KV head) units of one step, {passes} pass(es), "
+                      f"{el:.1f} s, fp64 numpy single thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (default 2)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    from paper_2606_06256_amd import inputs as I
+    wl = I.config(args.workload)
+
+    # CPU baseline first, before anything initialises the GPU
+    cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
+
+    import torch
+    from paper_2606_06256_amd import binding, build_lib
+    from paper_2606_06256_amd.device import DeviceWorkload
+    if not os.path.exists(binding.LIB_PATH):
+        build_lib.build()
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+
+    dw = DeviceWorkload(wl)
+    summary_ms = None
+    if wl.spec.sel_mode == I.SEL_TOPK_MEANKEY:
+        # page key sums are built once when pages are written; timed on their own
+        dw.summary()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            dw.summary()
+        e1.record()
+        torch.cuda.synchronize()
+        summary_ms = e0.elapsed_time(e1) / 3
+
+    for _ in range(args.warmup):
+        dw.step()
+    torch.cuda.synchronize()
+    ind, pages = dw.selection()
+    tokens, abytes = algorithmic_bytes(wl, ind, pages)
+
+    # timed region: exactly K steps
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        dw.step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(stop) / args.steps
+
+    # per-kernel launch times (HIP events around each launch, on its stream)
+    binding.profile_begin()
+    for _ in range(args.steps):
+        dw.step()
+    torch.cuda.synchronize()
+    prof = binding.profile_end()
+    n_attn, ms_attn = prof["decode_attn"]
+    attn_ms = ms_attn / n_attn
+    achieved = abytes / (attn_ms * 1e-3) / 1e9
+
+    roofline = {"kernel": "decode_attn", "bound": "hbm", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": None, "bytes_per_launch": abytes, "launch_ms": round(attn_ms, 5)}
+    if wl.max_q_len * wl.G > 16:
+        flops = attention_flops(wl, ind, pages)
+        roofline["mfma_tflops"] = round(flops / (attn_ms * 1e-3) / 1e12, 2)
+        roofline["mfma_frac"] = round(flops / (attn_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+    kernels = {k: {"launches": n, "mean_ms": round(t / n, 5)} for k, (n, t) in prof.items()}
+    line = {
+        "metric": METRIC,
+        "value": round(tokens / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.spec.name, "description": wl.spec.description,
+                   "requests": wl.B, "q_heads": wl.Hq, "kv_heads": wl.Hkv, "head_dim": wl.D,
+                   "page_size": wl.P, "segment_tokens": wl.spec.seg_tokens,
+                   "attended_kv_tokens_per_step": tokens,
+                   "step_gbs": round(abytes / (ms_per_step * 1e-3) / 1e9, 1),
+                   "kernels": kernels},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    if summary_ms is not None:
+        line["config"]["page_summary_ms"] = round(summary_ms, 4)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

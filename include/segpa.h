@@ -1,0 +1,239 @@
+/*
+ * segpa.h - SegPagedAttention with per-head page selection on AMD MI355X (gfx950).
+ *
+ * C ABI of libsegpa.so. Every pointer argument marked "device" is a HIP device
+ * pointer; every size and scalar is host data. The library never allocates,
+ * frees or retains caller memory past a call, except that the optional
+ * profiling hooks keep host-side event records between
+ * seg_paged_attn_profile_begin and seg_paged_attn_profile_end.
+ *
+ * What is computed follows RedKnot (arXiv 2606.06256):
+ *   - Section 4.3 and Algorithm 2 (SegPagedAttention): the KV cache of one
+ *     layer is stored per KV head as head segments; a segment maps to
+ *     consecutive virtual pages (segment table) and each virtual page to a
+ *     physical page (page table). Each KV head attends only to its own selected
+ *     page list, in one fused launch over all heads, without a mask.
+ *   - Algorithm 2, policy step: a global head keeps the full page range; a
+ *     local head keeps sink pages and recent-window pages, where the window of
+ *     query position i is W(i) = S_sink U [max(0, i - w), i] (Section 4.2).
+ *   - Section 4.4: attention over a key set split into parts, merged with
+ *     log-sum-exp, equals attention over the union (used for split-KV).
+ *
+ * Terms.
+ *   B = num_requests, Hq = num_q_heads, Hkv = num_kv_heads, G = Hq / Hkv,
+ *   D = head_dim, P = page_size, pps = pages_per_segment.
+ *   A unit is one (request r, KV head g) head stream, index u = r * Hkv + g.
+ *   Query head h reads KV head h / G.
+ *   ctx_lens[r] = L_r is the number of KV tokens of request r including its
+ *   current query chunk; the stream has n_pages(r) = ceil(L_r / P) logical
+ *   pages, page j holding tokens j*P .. j*P+P-1 (the last page may be partial).
+ *   Request r has n_q(r) = q_indptr[r+1] - q_indptr[r] query tokens; query i of
+ *   the chunk sits at position L_r - n_q(r) + i and sees selected tokens at
+ *   positions <= its own (causal, aligned to the end of the context).
+ *
+ * Translate (Algorithm 2): logical page j of unit (r, g) lives in segment
+ *   s = j / pps at offset o = j % pps;
+ *   virtual = seg_table[(r * Hkv + g) * max_segments + s] + o  (entry -1: unmapped)
+ *   physical = page_table[virtual].
+ *
+ * Physical page layout (both pools bf16, page stride P * D elements, 16-byte
+ * aligned base): a page holds P/16 tiles of 16 tokens; tile t of a page starts
+ * at element t * 16 * D.
+ *   K tile: [D/8][16][8]  element (token u, dim d) at ((d / 8) * 16 + u) * 8 + d % 8
+ *   V tile: [D][16]       element (token u, dim d) at d * 16 + u
+ * These are the operand layouts of the gfx950 matrix-core instructions used by
+ * the kernels, so every tile arrives in registers with contiguous loads.
+ *
+ * Selected pages: CSR over units. sel_indptr[u] .. sel_indptr[u+1]-1 index
+ * sel_pages, which holds logical page ids, strictly ascending within a unit and
+ * < n_pages(r). A unit with no pages is legal: its outputs are O = 0 and
+ * LSE = -inf. Pages that are not selected never enter the softmax (true
+ * eviction, Section 5.4).
+ *
+ * Outputs: out bf16 [total_q, Hq, D] (round to nearest even), with
+ * total_q = q_indptr[B]; lse fp32 [total_q, Hq], natural log of the softmax
+ * denominator including the max (may be NULL). MergeHeads of Algorithm 2 is the
+ * identity in this layout.
+ *
+ * Execution. All calls except seg_paged_attn_validate are asynchronous and
+ * stream-ordered on `stream` (a hipStream_t; NULL = the null stream): results
+ * are valid when the stream reaches the end of the call. Host-checkable
+ * argument errors return before anything is launched. Kernels never read out
+ * of bounds on bad table or list contents: an out-of-range page id, unmapped
+ * segment or out-of-range physical page is skipped (contributes nothing);
+ * seg_paged_attn_validate reports such data synchronously. Calls that share a
+ * workspace must not overlap.
+ */
+#ifndef SEGPA_H
+#define SEGPA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPA_OK = 0,
+  SPA_ERR_INVALID_ARG = -1,  /* null pointer, bad dimension, inconsistent sizes */
+  SPA_ERR_UNSUPPORTED = -2,  /* valid but not implemented here (e.g. D not 64/128) */
+  SPA_ERR_WORKSPACE = -3,    /* workspace null or smaller than required */
+  SPA_ERR_CAPACITY = -4,     /* sel_capacity below B * Hkv * max_segments * pps */
+  SPA_ERR_HIP = -5,          /* a HIP runtime call or launch failed */
+  SPA_ERR_BAD_DATA = -6      /* validate(): table or page-list content is invalid */
+} spa_status_t;
+
+/* Largest B * Hkv per call. */
+#define SPA_MAX_UNITS 8192
+
+typedef struct {
+  int32_t num_requests;       /* B >= 1 */
+  int32_t num_q_heads;        /* Hq, a multiple of Hkv, Hq / Hkv <= 16 */
+  int32_t num_kv_heads;       /* Hkv >= 1 */
+  int32_t head_dim;           /* D: 64 or 128 */
+  int32_t page_size;          /* P: 16, 32, 64, 128 or 256 tokens */
+  int32_t pages_per_segment;  /* pps >= 1 */
+  int32_t max_segments;       /* inner dimension of seg_table, >= 1 */
+  int32_t max_q_len;          /* host upper bound of n_q(r) over all requests, >= 1 */
+  int32_t total_q;            /* rows of q and out (= q_indptr[B]), >= 0 */
+  int32_t reserved0;
+  int64_t num_virtual_pages;  /* length of page_table */
+  int64_t num_phys_pages;     /* pages in each pool */
+  float softmax_scale;        /* <= 0 selects 1 / sqrt(D) */
+} spa_dims_t;
+
+typedef enum {
+  SPA_SEL_ALL = 0,          /* every page: U_h = V_h (global head of Algorithm 2) */
+  SPA_SEL_HEAD_CLASS = 1,   /* Algorithm 2 policy: global -> all pages; local -> pages
+                               overlapping S_sink or any W(i) of the chunk's queries */
+  SPA_SEL_RANDOM_HASH = 2,  /* forced pages + the other pages with the smallest
+                               SplitMix64 keys (seeded sample without replacement) */
+  SPA_SEL_TOPK_MEANKEY = 3  /* forced pages + the other pages with the highest
+                               score (q_bar . ksum_p) / n_valid(p), q_bar = sum of the
+                               G query heads of the request's last query token */
+} spa_sel_mode_t;
+
+typedef struct {
+  int32_t mode;               /* spa_sel_mode_t */
+  int32_t n_sink_tokens;      /* HEAD_CLASS: |S_sink|, the first positions of the stream */
+  int32_t window_tokens;      /* HEAD_CLASS: w */
+  int32_t forced_head_pages;  /* RANDOM_HASH/TOPK: pages 0 .. f-1 always selected */
+  int32_t forced_tail_pages;  /* RANDOM_HASH/TOPK: the last f pages always selected */
+  int32_t reserved;
+  uint64_t seed;              /* RANDOM_HASH */
+  const int8_t* head_policy;  /* HEAD_CLASS: device [Hkv], 1 = global, 0 = local */
+  const int32_t* budget_pages;/* RANDOM_HASH/TOPK: device [B], pages per unit of request r */
+} spa_select_params_t;
+
+/*
+ * Bytes of workspace that seg_paged_attn_select (for `sel_mode`) and
+ * seg_paged_attn_fwd need for these dims on the current device. Returns 0 on
+ * invalid dims. The workspace is scratch owned by the caller; its content
+ * between calls does not matter.
+ */
+size_t seg_paged_attn_workspace_size(const spa_dims_t* dims, int32_t sel_mode);
+
+/*
+ * SelectVisibleState (Section 4.4 adapter interface; Algorithm 2 policy,
+ * Translate-ready metadata): the selected logical pages of every unit.
+ *
+ * Count of unit u (request r, KV head g), n = n_pages(r):
+ *   ALL: n.  HEAD_CLASS: global n; local |[0, ceil(min(n_sink, L)/P)) U
+ *   [floor(max(0, L - n_q - w) / P), n)|.  RANDOM_HASH / TOPK:
+ *   min(n, max(budget_pages[r], |forced|)), forced = [0, fh) U [n - ft, n).
+ * RANDOM_HASH key of page p: sm(sm(seed) ^ (r << 40 | g << 32 | p)) with
+ *   sm(x) = SplitMix64 output function applied to x + 0x9E3779B97F4A7C15;
+ *   smaller keys first, equal keys to the lower index.
+ * TOPK_MEANKEY score in float64 from page_ksum (see page_summary); higher
+ *   first, equal scores to the lower index. page_ksum may be NULL otherwise.
+ *
+ * In:  ctx_lens device [B]; q device bf16 [total_q, Hq, D] and q_indptr device
+ *      [B+1] (q is read by TOPK only; q_indptr by HEAD_CLASS and TOPK, may be
+ *      NULL for ALL/RANDOM_HASH); seg_table device [B*Hkv*max_segments];
+ *      page_table device [num_virtual_pages] (both read by TOPK only).
+ * Out: sel_indptr device [B*Hkv+1]; sel_pages device [sel_capacity], logical
+ *      ids ascending per unit. sel_capacity must be at least
+ *      B * Hkv * max_segments * pps.
+ * ctx_lens[r] must not exceed max_segments * pps * P (larger values are
+ * clamped to that many pages).
+ */
+spa_status_t seg_paged_attn_select(const spa_dims_t* dims, const spa_select_params_t* params,
+                                   const int32_t* ctx_lens, const void* q, const int32_t* q_indptr,
+                                   const float* page_ksum, const int32_t* seg_table,
+                                   const int32_t* page_table, int32_t* sel_indptr,
+                                   int32_t* sel_pages, int64_t sel_capacity, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+/*
+ * Execute / FusedVarlenAttention + MergeHeads (Algorithm 2): softmax attention
+ * of every query row over the selected pages of its unit, in one fused launch
+ * over all units, then a log-sum-exp combine of split partial results
+ * (Section 4.4). bf16 inputs, fp32 accumulation, bf16 output.
+ *
+ * In:  q device bf16 [total_q, Hq, D]; q_indptr device [B+1]; ctx_lens device
+ *      [B]; k_pool, v_pool device bf16 [num_phys_pages, P * D] in the tile
+ *      layout above; seg_table device [B*Hkv*max_segments]; page_table device
+ *      [num_virtual_pages]; sel_indptr device [B*Hkv+1]; sel_pages device
+ *      [sel_capacity] (entries past sel_capacity are never read).
+ * Out: out device bf16 [total_q, Hq, D]; lse device fp32 [total_q, Hq] or NULL.
+ * Shapes: max_q_len * G <= 16 runs the decode kernel (one matrix-core tile of
+ * query rows per unit); larger chunks run the chunked-prefill kernel.
+ */
+spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int32_t* q_indptr,
+                                const int32_t* ctx_lens, const void* k_pool, const void* v_pool,
+                                const int32_t* seg_table, const int32_t* page_table,
+                                const int32_t* sel_indptr, const int32_t* sel_pages,
+                                int64_t sel_capacity, void* out, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/*
+ * Page key summary for TOPK_MEANKEY (this build's content rule; the paper
+ * states none): page_ksum[p][d] = float32 rounding of the sum over the first
+ * page_valid_tokens[p] tokens of physical page p of K[token][d], accumulated in
+ * float64 (exact when the page's nonzero magnitudes span less than 2^40).
+ * In:  k_pool device bf16 [num_phys_pages, P * D]; page_valid_tokens device
+ *      int32 [num_phys_pages] (0..P; values outside are clamped).
+ * Out: page_ksum device fp32 [num_phys_pages, D].
+ */
+spa_status_t seg_paged_attn_page_summary(const spa_dims_t* dims, const void* k_pool,
+                                         const int32_t* page_valid_tokens, float* page_ksum,
+                                         void* stream);
+
+/*
+ * Synchronous check of table and list contents (debug aid). Checks q_indptr
+ * (monotone, n_q <= min(max_q_len, L)), ctx_lens (0 <= L <= max_segments*pps*P),
+ * sel_indptr (starts at 0, monotone), every selected page (in [0, n_pages),
+ * strictly ascending in its unit, segment mapped, virtual page in range,
+ * physical page in range). Returns SPA_OK or SPA_ERR_BAD_DATA; *bad_code (may
+ * be NULL) receives a nonzero code naming the first failed check class and
+ * *bad_index the smallest offending index of that class. Needs 64 bytes of
+ * workspace.
+ */
+spa_status_t seg_paged_attn_validate(const spa_dims_t* dims, const int32_t* ctx_lens,
+                                     const int32_t* q_indptr, const int32_t* seg_table,
+                                     const int32_t* page_table, const int32_t* sel_indptr,
+                                     const int32_t* sel_pages, int64_t sel_capacity,
+                                     int32_t* bad_code,
+                                     int64_t* bad_index, void* workspace, size_t workspace_bytes,
+                                     void* stream);
+
+/* Static text for a status code. */
+const char* seg_paged_attn_status_string(spa_status_t status);
+
+/*
+ * Optional per-kernel timing (measurement aid, not thread-safe). Between begin
+ * and end every kernel launch of the library is bracketed by HIP events on the
+ * launch stream. end() waits for those events and fills, for up to `cap`
+ * kernel kinds, the kind name (static string), the number of launches and the
+ * summed milliseconds; it returns the number of kinds (or < 0 on error).
+ */
+spa_status_t seg_paged_attn_profile_begin(void);
+int32_t seg_paged_attn_profile_end(const char** names, int32_t* launches, double* total_ms,
+                                   int32_t cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEGPA_H */

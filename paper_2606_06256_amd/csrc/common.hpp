@@ -1,0 +1,92 @@
+// Shared device helpers for the SegPagedAttention kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.hpp"
+
+namespace segpa {
+
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// Matrix-core steps. Lane layouts (gfx950, checked on hardware):
+//   16x16x32 bf16: A[i = l%16][k = 8*(l/16) + e], B[k = 8*(l/16) + e][j = l%16]
+//   16x16x16 bf16: A[i = l%16][k = 4*(l/16) + e], B[k = 4*(l/16) + e][j = l%16]
+//   result (both): C[i = 4*(l/16) + r][j = l%16], r = 0..3
+__device__ __forceinline__ f32x4 mfma16x16x32(s16x8 a, s16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16x16x16(s16x4 a, s16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+// Four floats -> four bf16 (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ s16x4 pack_bf16x4(float a, float b, float c, float d) {
+  bf16x4 v;
+  v.x = (__bf16)a;
+  v.y = (__bf16)b;
+  v.z = (__bf16)c;
+  v.w = (__bf16)d;
+  return __builtin_bit_cast(s16x4, v);
+}
+
+__device__ __forceinline__ float bf16_bits_to_float(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// Buffer resource (V#) for raw buffer loads on gfx9-family parts: base
+// address, no stride, `bytes` of range (reads past it return 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <typename T>
+__device__ __forceinline__ T clampv(T x, T lo, T hi) {
+  return x < lo ? lo : (x > hi ? hi : x);
+}
+
+// Algorithm 2, Translate: logical page j of one head stream -> physical page.
+// Returns -1 for anything out of range (the page is then skipped).
+__device__ __forceinline__ int translate_page(const int32_t* __restrict__ seg_row,
+                                              const int32_t* __restrict__ page_table, int j,
+                                              int pps, int max_segs, int64_t n_virtual,
+                                              int64_t n_phys) {
+  if (j < 0) return -1;
+  const int s = j / pps;
+  const int o = j - s * pps;
+  if (s >= max_segs) return -1;
+  const int v0 = seg_row[s];
+  if (v0 < 0) return -1;
+  const int64_t v = (int64_t)v0 + o;
+  if (v >= n_virtual) return -1;
+  const int ph = page_table[v];
+  if (ph < 0 || (int64_t)ph >= n_phys) return -1;
+  return ph;
+}
+
+// SplitMix64 (Steele, Lea, Flood, OOPSLA 2014): output function, and one
+// generator output from a state (advance by the golden gamma, then mix).
+__device__ __forceinline__ uint64_t splitmix64_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+__device__ __forceinline__ uint64_t splitmix64(uint64_t state) {
+  return splitmix64_mix(state + 0x9E3779B97F4A7C15ull);
+}
+
+// Wave-wide inclusive/exclusive counts of a predicate, in lane order.
+__device__ __forceinline__ int lane_prefix_count(uint64_t ballot) {
+  const int lane = __lane_id();
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  return __popcll(ballot & below);
+}
+
+}  // namespace segpa

@@ -1,0 +1,94 @@
+// Kernel argument blocks and host-side launchers (internal to libsegpa.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace segpa {
+
+constexpr int kTile = 16;       // tokens per KV tile; a page holds P / 16 tiles
+constexpr int kWave = 64;
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr float kLog2e = 1.44269504088896340736f;
+
+// Forward pass (decode split-KV kernel, combine kernel, prefill kernel).
+struct FwdArgs {
+  const __bf16* q;            // [total_q, Hq, D]
+  const int32_t* q_indptr;    // [B+1]
+  const int32_t* ctx_lens;    // [B]
+  const __bf16* k_pool;       // [n_phys, P*D], tile layout
+  const __bf16* v_pool;
+  const int32_t* seg_table;   // [B*Hkv*max_segs]
+  const int32_t* page_table;  // [n_virtual]
+  const int32_t* sel_indptr;  // [units+1]
+  const int32_t* sel_pages;   // [sel_capacity]
+  __bf16* out;                // [total_q, Hq, D]
+  float* lse;                 // [total_q, Hq] or null
+  float* part_o;              // workspace: [slots][16][D] normalised split outputs
+  float* part_lse;            // workspace: [slots][16] base-2 LSE of each split
+                              // (slots = total_waves + units * row_blocks)
+  int64_t n_virtual;
+  int64_t n_phys;
+  int64_t sel_capacity;
+  int32_t B, Hq, Hkv, G, D, P;
+  int32_t tpp_log2;           // log2(P / 16)
+  int32_t pps, max_segs, units, max_q_len, total_q;
+  int32_t total_waves;        // decode: waves of the split-KV launch
+  int32_t row_blocks;         // query-row blocks of 16 per unit: ceil(max_q_len * G / 16)
+  float scale_log2;           // softmax scale * log2(e)
+};
+
+// Page selection.
+struct SelArgs {
+  const int32_t* ctx_lens;
+  const int32_t* q_indptr;
+  const __bf16* q;
+  const float* page_ksum;     // [n_phys, D] (TOPK)
+  const int32_t* seg_table;
+  const int32_t* page_table;
+  const int8_t* head_policy;  // [Hkv] (HEAD_CLASS)
+  const int32_t* budget;      // [B] (RANDOM_HASH / TOPK)
+  int32_t* sel_indptr;        // [units+1]
+  int32_t* sel_pages;         // [capacity]
+  uint64_t* score_keys;       // workspace [units][max_pages] (TOPK)
+  uint64_t seed;
+  int64_t n_virtual, n_phys, capacity;
+  int32_t mode, B, Hq, Hkv, G, D, P, pps, max_segs, units, max_pages, total_q;
+  int32_t n_sink, window, forced_head, forced_tail;
+};
+
+struct SummaryArgs {
+  const __bf16* k_pool;
+  const int32_t* page_valid;
+  float* page_ksum;
+  int64_t n_phys;
+  int32_t D, P;
+};
+
+struct ValidateArgs {
+  const int32_t* ctx_lens;
+  const int32_t* q_indptr;
+  const int32_t* seg_table;
+  const int32_t* page_table;
+  const int32_t* sel_indptr;
+  const int32_t* sel_pages;
+  unsigned long long* result;  // [4]: per check class, smallest bad index (init ~0)
+  int64_t n_virtual, n_phys, capacity;
+  int32_t B, Hkv, P, pps, max_segs, max_q_len, total_q, units;
+};
+
+constexpr int kDecodeBlock = 256;   // 4 waves
+constexpr int kSelectBlock = 512;
+constexpr int kSelectKeyCache = 4096;  // keys held in LDS by the select kernel
+
+hipError_t launch_decode(const FwdArgs& a, hipStream_t stream);
+hipError_t launch_combine(const FwdArgs& a, hipStream_t stream);
+int decode_blocks_per_cu(int D, int units);
+
+hipError_t launch_select_scores(const SelArgs& a, hipStream_t stream);
+hipError_t launch_select_fill(const SelArgs& a, hipStream_t stream);
+
+hipError_t launch_page_summary(const SummaryArgs& a, hipStream_t stream);
+hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);
+
+}  // namespace segpa

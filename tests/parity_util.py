@@ -1,0 +1,162 @@
+"""Helpers for GPU-vs-oracle parity (imported by the GPU tests and smoke()).
+
+The oracle's inputs come from the seeded generator on the CPU; its selection
+and its outputs are computed by the oracle alone. The GPU path gets the same
+seeded inputs on the device.
+
+Tolerances: outputs within max-abs 2e-2 and mean-abs 2e-3 (bf16 inputs, fp32
+accumulation, bf16 output); LSE within 1e-3 absolute (the scores are exact bf16
+products accumulated in fp32, relative error ~1e-6, so the log-sum-exp error is
+far below 1e-3); page selections bit-exact, except that TOPK pages whose exact
+score lies within 1e-12 (relative) of the k-th score may be exchanged (both
+choices are correct at float64 resolution).
+"""
+from __future__ import annotations
+
+import math
+import os
+import sys
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from oracle import segpa_oracle as O  # noqa: E402
+from paper_2606_06256_amd import inputs as I  # noqa: E402
+
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+LSE_ABS = 1e-3
+TIE_REL = 1e-12
+
+
+def kv64(wl: I.Workload, r: int, g: int):
+    K, V = wl.unit_kv(r, g, "cpu")
+    return K.double().numpy(), V.double().numpy()
+
+
+def oracle_selection(wl: I.Workload, q64: np.ndarray, units=None) -> dict:
+    sp = wl.spec
+    return O.select(sp.sel_mode, wl.ctx_lens, wl.q_indptr, wl.Hq, wl.Hkv, wl.P,
+                    budgets=wl.budgets, forced_head=sp.forced_head, forced_tail=sp.forced_tail,
+                    seed=sp.sel_seed, head_policy=wl.head_policy, n_sink=sp.n_sink,
+                    window=sp.window, q=q64, kv_of_unit=lambda r, g: kv64(wl, r, g), units=units)
+
+
+def topk_tie_ok(wl: I.Workload, q64: np.ndarray, u: int, got, want) -> bool:
+    """A differing TOPK list is acceptable only by exchanges at the k-th score."""
+    sp = wl.spec
+    r, g = divmod(u, wl.Hkv)
+    K, _ = kv64(wl, r, g)
+    ksum, valid = O.unit_key_sums(K, wl.P)
+    last = int(wl.q_indptr[r + 1]) - 1
+    _, scores = O.pages_topk_meankey(q64[last, g * wl.G:(g + 1) * wl.G], ksum, valid,
+                                     int(wl.budgets[r]), sp.forced_head, sp.forced_tail)
+    want_s = set(want)
+    if len(got) != len(want) or len(set(got)) != len(got):
+        return False
+    thr = min(scores[p] for p in want_s) if want_s else 0
+    for p in set(got) ^ want_s:
+        if abs(float(scores[p] - thr)) > TIE_REL * max(abs(float(thr)), 1e-300):
+            return False
+    return True
+
+
+def compare_selection(wl, dw, q64, want: dict) -> list:
+    """Bit-exact page lists; returns units whose lists differ by valid TOPK ties."""
+    ind, pages = dw.selection()
+    assert ind[0] == 0
+    ties = []
+    for u, w in want.items():
+        got = pages[ind[u]:ind[u + 1]].tolist()
+        if got == list(w):
+            continue
+        if wl.spec.sel_mode == I.SEL_TOPK_MEANKEY and topk_tie_ok(wl, q64, u, got, list(w)):
+            ties.append(u)
+            continue
+        raise AssertionError(f"unit {u}: selection differs (got {len(got)} pages, want {len(w)}); "
+                             f"first diff {[(a, b) for a, b in zip(got, w) if a != b][:3]}")
+    return ties
+
+
+class ErrStats:
+    def __init__(self):
+        self.max_abs = 0.0
+        self.sum_abs = 0.0
+        self.n = 0
+        self.lse_max = 0.0
+
+    def add(self, got: np.ndarray, want: np.ndarray, lse_got: np.ndarray, lse_want: np.ndarray):
+        d = np.abs(got - want)
+        self.max_abs = max(self.max_abs, float(d.max()) if d.size else 0.0)
+        self.sum_abs += float(d.sum())
+        self.n += d.size
+        inf_w = ~np.isfinite(lse_want)
+        assert np.array_equal(inf_w, ~np.isfinite(lse_got)), "LSE -inf pattern differs"
+        if np.any(~inf_w):
+            self.lse_max = max(self.lse_max, float(np.max(np.abs(lse_got[~inf_w] - lse_want[~inf_w]))))
+
+    @property
+    def mean_abs(self):
+        return self.sum_abs / max(1, self.n)
+
+    def check(self, what=""):
+        assert self.max_abs <= MAX_ABS, f"{what}: max-abs {self.max_abs:.3e} > {MAX_ABS}"
+        assert self.mean_abs <= MEAN_ABS, f"{what}: mean-abs {self.mean_abs:.3e} > {MEAN_ABS}"
+        assert self.lse_max <= LSE_ABS, f"{what}: LSE error {self.lse_max:.3e} > {LSE_ABS}"
+
+    def __repr__(self):
+        return f"max_abs={self.max_abs:.3e} mean_abs={self.mean_abs:.3e} lse={self.lse_max:.3e} n={self.n}"
+
+
+def compare_outputs(wl, dw, q64, sel: dict, units, stats: ErrStats = None) -> ErrStats:
+    stats = stats or ErrStats()
+    out = dw.out.float().cpu().numpy()
+    lse = dw.lse.cpu().numpy()
+    G = wl.G
+    for u in units:
+        r, g = divmod(u, wl.Hkv)
+        q0, q1 = int(wl.q_indptr[r]), int(wl.q_indptr[r + 1])
+        if q1 == q0:
+            continue
+        K, V = kv64(wl, r, g)
+        Oo, LSE = O.forward_unit(q64, wl.q_indptr, wl.ctx_lens, wl.Hq, wl.Hkv, wl.P, u, sel[u], K, V)
+        stats.add(out[q0:q1, g * G:(g + 1) * G], Oo, lse[q0:q1, g * G:(g + 1) * G], LSE)
+    return stats
+
+
+def sample_units(U: int, k: int = 4) -> list:
+    if U <= k:
+        return list(range(U))
+    return sorted({0, U - 1, *[int(x) for x in np.linspace(0, U - 1, k)[1:-1]]})
+
+
+def run_parity(wl, *, units=None, sel_units=None, device="cuda", label=""):
+    """Select + fwd on the GPU; compare selections (units in sel_units, default
+    all) and outputs (units, default all) with the oracle."""
+    from paper_2606_06256_amd.device import DeviceWorkload
+
+    print(f"[parity] {label or wl.spec.name}: B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} "
+          f"P={wl.P} mode={wl.spec.sel_mode}", flush=True)
+    dw = DeviceWorkload(wl, device)
+    if wl.spec.sel_mode == I.SEL_TOPK_MEANKEY:
+        dw.summary()
+    dw.select()
+    dw.fwd()
+    torch.cuda.synchronize()
+    q64 = wl.q("cpu").double().numpy()
+    U = wl.num_units
+    sel_units = list(range(U)) if sel_units is None else sel_units
+    want = oracle_selection(wl, q64, units=sel_units)
+    ties = compare_selection(wl, dw, q64, want)
+    units = list(range(U)) if units is None else units
+    extra = [u for u in units if u not in want]
+    if extra:
+        want.update(oracle_selection(wl, q64, units=extra))
+    stats = compare_outputs(wl, dw, q64, want, [u for u in units if u not in ties])
+    print(f"[parity] {label or wl.spec.name}: {stats} ties={len(ties)}", flush=True)
+    stats.check(label or wl.spec.name)
+    return dw, stats

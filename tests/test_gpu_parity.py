@@ -1,0 +1,238 @@
+"""GPU parity: the HIP path through the C-ABI against the fp64 oracle.
+
+Sizes the oracle finishes in seconds that still span many tiles, several
+waves per unit and ragged tails; then every named workload at full size in
+the benchmark's launch configuration, on sampled units. Each case prints
+its name before it touches the GPU.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_06256_amd import inputs as I
+from paper_2606_06256_amd.device import DeviceWorkload
+
+import parity_util as PU
+
+pytestmark = pytest.mark.gpu
+
+
+def _require_gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+
+
+def _spec(**kw):
+    base = dict(name="edge", B=2, Hq=8, Hkv=2, D=128, P=16, seg_tokens=256, ctx_lens=[700, 333],
+                q_lens=[1, 1], seed=4242)
+    base.update(kw)
+    return I.Spec(**base)
+
+
+# --------------------------------------------------------------------------
+# the named workloads, scaled down (all units compared)
+# --------------------------------------------------------------------------
+def test_tiny_config_full():
+    _require_gpu()
+    PU.run_parity(I.config(1), label="tiny")
+
+
+@pytest.mark.parametrize("i,div,batch", [(2, 16, 4), (3, 32, 6), (5, 32, 3)])
+def test_scaled_decode_configs(i, div, batch):
+    _require_gpu()
+    PU.run_parity(I.build(I.scaled_spec(i, div, batch)), label=f"cfg{i}/div{div}")
+
+
+def test_scaled_prefill_config():
+    _require_gpu()
+    sp = I.scaled_spec(4, 32, 2)
+    sp.q_lens = [48, 31]
+    sp.ctx_lens = [2048 + 48, 1500 + 31]
+    sp.budgets = [40, 30]
+    sp.forced_tail = 3
+    PU.run_parity(I.build(sp), label="cfg4/small")
+
+
+# --------------------------------------------------------------------------
+# shapes and edge cases
+# --------------------------------------------------------------------------
+EDGE = {
+    "mha_d64": dict(Hq=4, Hkv=4, D=64),
+    "gqa2": dict(Hq=4, Hkv=2),
+    "gqa8": dict(Hq=16, Hkv=2),
+    "gqa16": dict(Hq=32, Hkv=2),
+    "page32": dict(P=32, seg_tokens=256),
+    "page64_d64": dict(P=64, seg_tokens=512, D=64),
+    "ctx_below_page": dict(ctx_lens=[5, 1]),
+    "single_page": dict(ctx_lens=[16, 16]),
+    "multi_query_causal": dict(q_lens=[3, 4], ctx_lens=[300, 129]),
+    "chunk_g8": dict(Hq=16, Hkv=2, q_lens=[2, 2]),
+    "rows_cross_blocks": dict(Hq=24, Hkv=2, q_lens=[5, 3], ctx_lens=[400, 64]),
+    "random_forced": dict(sel_mode=I.SEL_RANDOM_HASH, budgets=[9, 4], forced_head=2, forced_tail=3,
+                          sel_seed=77),
+    "random_zero_budget": dict(sel_mode=I.SEL_RANDOM_HASH, budgets=[0, 2], sel_seed=5),
+    "topk_p32": dict(sel_mode=I.SEL_TOPK_MEANKEY, P=32, budgets=[5, 3], shift_pages=2,
+                     shift_mag=3.0),
+    "topk_partial": dict(sel_mode=I.SEL_TOPK_MEANKEY, budgets=[7, 30], forced_tail=1,
+                         ctx_lens=[701, 333]),
+    "head_class": dict(sel_mode=I.SEL_HEAD_CLASS, Hkv=4, Hq=8, head_policy=[1, 0, 0, 1],
+                       n_sink=4, window=100, ctx_lens=[1001, 300]),
+    "head_class_chunk": dict(sel_mode=I.SEL_HEAD_CLASS, Hkv=2, Hq=4, head_policy=[0, 1],
+                             n_sink=20, window=40, q_lens=[6, 2], ctx_lens=[900, 70]),
+    "aliased_prefix": dict(B=3, ctx_lens=[600, 512, 300], q_lens=[1, 1, 1],
+                           shared_prefix_segments=1),
+    "spare_phys_pages": dict(extra_phys_pages=37),
+    "scaled_keys": dict(k_page_scale_sigma=0.5, sel_mode=I.SEL_RANDOM_HASH, budgets=[20, 10]),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_edge_cases(name):
+    _require_gpu()
+    PU.run_parity(I.build(_spec(name=name, **EDGE[name])), label=name)
+
+
+def test_many_units_short_lists():
+    _require_gpu()
+    B = 40
+    rng = np.random.default_rng(8)
+    ctx = rng.integers(1, 200, size=B).tolist()
+    sp = _spec(name="many_units", B=B, Hq=8, Hkv=4, ctx_lens=ctx, q_lens=[1] * B,
+               sel_mode=I.SEL_RANDOM_HASH, budgets=rng.integers(0, 6, size=B).tolist(), sel_seed=3)
+    PU.run_parity(I.build(sp), label="many_units")
+
+
+def test_explicit_lists_with_empty_units():
+    _require_gpu()
+    wl = I.build(_spec(name="explicit", B=3, ctx_lens=[900, 40, 300], q_lens=[2, 1, 1]))
+    dw = DeviceWorkload(wl)
+    rng = np.random.default_rng(1)
+    lists = []
+    for u in range(wl.num_units):
+        r = u // wl.Hkv
+        n = int(wl.n_pages[r])
+        k = 0 if u % 3 == 1 else int(rng.integers(1, n + 1))
+        lists.append(sorted(rng.choice(n, size=k, replace=False).tolist()))
+    dw.set_selection(lists)
+    dw.fwd()
+    torch.cuda.synchronize()
+    q64 = wl.q("cpu").double().numpy()
+    stats = PU.compare_outputs(wl, dw, q64, dict(enumerate(lists)), range(wl.num_units))
+    print("[parity] explicit lists:", stats, flush=True)
+    stats.check("explicit")
+    lse = dw.lse.cpu().numpy()
+    assert np.all(np.isneginf(lse[:2, 4:8]))           # request 0, KV head 1: empty list
+    assert np.all(dw.out.float().cpu().numpy()[:2, 4:8] == 0)
+
+
+# --------------------------------------------------------------------------
+# invariances of the GPU path
+# --------------------------------------------------------------------------
+def test_split_count_invariance_and_determinism(monkeypatch):
+    _require_gpu()
+    wl = I.build(I.scaled_spec(2, 8, 4))
+    outs = []
+    for blocks in ("1", "3", "8"):
+        monkeypatch.setenv("SEGPA_DECODE_BLOCKS_PER_CU", blocks)
+        print(f"[split] blocks per CU {blocks}", flush=True)
+        dw = DeviceWorkload(wl)
+        dw.step()
+        dw.fwd()
+        torch.cuda.synchronize()
+        first = dw.out.clone()
+        dw.fwd()
+        torch.cuda.synchronize()
+        assert torch.equal(first, dw.out), "run-to-run results differ"
+        outs.append(first.float())
+        del dw
+    for o in outs[1:]:
+        assert float((o - outs[0]).abs().max()) <= 1e-2
+
+
+def test_physical_placement_invariance():
+    _require_gpu()
+    wl = I.build(_spec(name="placement", P=32, ctx_lens=[1200, 555], q_lens=[2, 1],
+                       sel_mode=I.SEL_RANDOM_HASH, budgets=[20, 9], sel_seed=11))
+    a = DeviceWorkload(wl)
+    a.step()
+    perm = torch.from_numpy(np.random.default_rng(2).permutation(wl.num_phys)).cuda()
+    b = DeviceWorkload(wl)
+    b.k_pool = torch.empty_like(a.k_pool)
+    b.v_pool = torch.empty_like(a.v_pool)
+    b.k_pool[perm] = a.k_pool
+    b.v_pool[perm] = a.v_pool
+    b.page_table = perm.to(torch.int32)[a.page_table.long()].contiguous()
+    b.step()
+    torch.cuda.synchronize()
+    assert torch.equal(a.sel_indptr, b.sel_indptr) and torch.equal(a.sel_pages, b.sel_pages)
+    assert torch.equal(a.out, b.out) and torch.equal(a.lse, b.lse)
+
+
+def test_page_summary_bit_exact():
+    _require_gpu()
+    from oracle import segpa_oracle as O
+    wl = I.build(_spec(name="ksum", P=32, ctx_lens=[1000, 77], sel_mode=I.SEL_TOPK_MEANKEY,
+                       budgets=[3, 2], shift_pages=3, shift_mag=3.0))
+    dw = DeviceWorkload(wl)
+    dw.summary()
+    torch.cuda.synchronize()
+    ks = dw.page_ksum.cpu().numpy()
+    for r in range(wl.B):
+        for g in range(wl.Hkv):
+            K, _ = PU.kv64(wl, r, g)
+            want, _ = O.unit_key_sums(K, wl.P)
+            got = ks[wl.unit_phys_pages(r, g)]
+            assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def test_generated_pool_matches_cpu_generation():
+    _require_gpu()
+    wl = I.build(I.scaled_spec(3, 16, 3))
+    dw = DeviceWorkload(wl)
+    kp, vp = dw.k_pool.cpu(), dw.v_pool.cpu()
+    for r in range(wl.B):
+        for g in (0, wl.Hkv - 1):
+            K, V = wl.unit_kv(r, g, "cpu")
+            kt, vt = wl.tile_unit(K, V, int(wl.n_pages[r]))
+            ph = torch.from_numpy(wl.unit_phys_pages(r, g).astype(np.int64))
+            assert torch.equal(kp[ph], kt) and torch.equal(vp[ph], vt)
+
+
+def test_validate_reports_bad_lists():
+    _require_gpu()
+    wl = I.build(_spec(name="validate", sel_mode=I.SEL_RANDOM_HASH, budgets=[10, 5], sel_seed=9))
+    dw = DeviceWorkload(wl)
+    dw.select()
+    st, code, idx = dw.validate()
+    assert (st, code) == (0, 0)
+    good = dw.sel_pages.clone()
+    n0 = int(wl.n_pages[0])
+    dw.sel_pages[3] = n0 + 5                    # page id past the context
+    st, code, idx = dw.validate()
+    assert st == -6 and code == 4 and idx == 3
+    dw.fwd()                                    # never faults: the bad page is skipped
+    torch.cuda.synchronize()
+    dw.sel_pages.copy_(good)
+    dw.sel_pages[2], dw.sel_pages[3] = good[3], good[2]   # not ascending
+    st, code, idx = dw.validate()
+    assert st == -6 and code == 4 and idx in (2, 3)
+    dw.sel_pages.copy_(good)
+    ind = dw.sel_indptr.clone()
+    dw.sel_indptr[1] = ind[2] + 1
+    st, code, idx = dw.validate()
+    assert st == -6 and code == 3
+
+
+# --------------------------------------------------------------------------
+# full-size workloads in the benchmark's launch configuration
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("i", [2, 3, 4, 5])
+def test_full_size_config(i):
+    _require_gpu()
+    wl = I.config(i)
+    U = wl.num_units
+    units = PU.sample_units(U, 3)
+    # selections: every unit for the seeded rules, sampled units for TOPK
+    sel_units = units if wl.spec.sel_mode == I.SEL_TOPK_MEANKEY else None
+    PU.run_parity(wl, units=units, sel_units=sel_units, label=f"cfg{i}/full")
