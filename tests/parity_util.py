@@ -33,9 +33,18 @@ LSE_ABS = 1e-3
 TIE_REL = 1e-12
 
 
+_KV_CACHE: dict = {}
+
+
 def kv64(wl: I.Workload, r: int, g: int):
-    K, V = wl.unit_kv(r, g, "cpu")
-    return K.double().numpy(), V.double().numpy()
+    """Logical K, V of unit (r, g) as float64, generated on the CPU (small cache)."""
+    key = (id(wl), r, g)
+    if key not in _KV_CACHE:
+        if len(_KV_CACHE) >= 6:
+            _KV_CACHE.pop(next(iter(_KV_CACHE)))
+        K, V = wl.unit_kv(r, g, "cpu")
+        _KV_CACHE[key] = (K.double().numpy(), V.double().numpy())
+    return _KV_CACHE[key]
 
 
 def oracle_selection(wl: I.Workload, q64: np.ndarray, units=None) -> dict:
