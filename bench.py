@@ -167,17 +167,24 @@ def main():
         dw.step()
     torch.cuda.synchronize()
     prof = binding.profile_end()
-    n_attn, ms_attn = prof["decode_attn"]
+    prefill = "prefill_attn" in prof
+    kname = "prefill_attn" if prefill else "decode_attn"
+    n_attn, ms_attn = prof[kname]
     attn_ms = ms_attn / n_attn
     achieved = abytes / (attn_ms * 1e-3) / 1e9
-
-    roofline = {"kernel": "decode_attn", "bound": "hbm", "achieved": round(achieved, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": None, "bytes_per_launch": abytes, "launch_ms": round(attn_ms, 5)}
-    if wl.max_q_len * wl.G > 16:
+    if prefill:
+        # the chunk's attention is a dense contraction: matrix-core bound
         flops = attention_flops(wl, ind, pages)
-        roofline["mfma_tflops"] = round(flops / (attn_ms * 1e-3) / 1e12, 2)
-        roofline["mfma_frac"] = round(flops / (attn_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+        tf = flops / (attn_ms * 1e-3) / 1e12
+        roofline = {"kernel": kname, "bound": "mfma", "achieved": round(tf, 2),
+                    "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                    "flops_per_launch": flops, "launch_ms": round(attn_ms, 5),
+                    "hbm_gbs": round(achieved, 1)}
+    else:
+        roofline = {"kernel": kname, "bound": "hbm", "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": None, "bytes_per_launch": abytes, "launch_ms": round(attn_ms, 5)}
     kernels = {k: {"launches": n, "mean_ms": round(t / n, 5)} for k, (n, t) in prof.items()}
     line = {
         "metric": METRIC,

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsegpa.so")
 
-SOURCES = ["api.cpp", "decode.hip", "select.hip", "summary.hip"]
+SOURCES = ["api.cpp", "decode.hip", "prefill.hip", "select.hip", "summary.hip"]
 ARCH = "gfx950"
 
 
@@ -36,9 +36,15 @@ def common_flags() -> list[str]:
             "-I", INCLUDE, "-I", CSRC]
 
 
+# per-source extra flags: matrix-core accumulators in ordinary VGPRs (the
+# decode kernel rescales them every tile; AGPR accumulators cost a copy each way)
+EXTRA = {"decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+         "prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     out = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *common_flags(), "-c", os.path.join(CSRC, src), "-o", out]
+    cmd = [hipcc(), *common_flags(), *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", out]
     if src.endswith(".cpp"):
         cmd.insert(1, "-xhip")
     r = subprocess.run(cmd, capture_output=True, text=True)

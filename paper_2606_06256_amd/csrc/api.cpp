@@ -71,8 +71,12 @@ int decode_waves(int D, int units) {
       cus < 1)
     return -1;
   if (waves < 0) {
-    // one resident wave per SIMD slot the kernel's registers allow
-    waves = cus * decode_blocks_per_cu(D, units) * (kDecodeBlock / kWave);
+    // One wave per SIMD (one block of 4 waves per compute unit), each with two
+    // tiles in flight. Measured on MI355X, this beats 2 or 3 waves per SIMD
+    // on every decode workload (fewer, longer stream shares: less start-up
+    // per byte and fewer partials to combine). Never more than the
+    // registers allow.
+    waves = cus * std::min(1, decode_blocks_per_cu(D, units)) * (kDecodeBlock / kWave);
     std::lock_guard<std::mutex> lk(g_dev_mu);
     g_decode_waves[key] = waves;
   }
@@ -275,6 +279,12 @@ spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int
   a.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
                                         align_up((size_t)slots * 16 * a.D * sizeof(float)));
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t rows = (int64_t)dims->max_q_len * a.G;
+  if (rows >= kPrefillMinRows) {
+    // chunked prefill: one block per (unit, row block), all selected keys, no split
+    a.row_blocks = (int)((rows + prefill_rows_per_block() - 1) / prefill_rows_per_block());
+    return hip_status(timed_launch("prefill_attn", s, [&] { return launch_prefill(a, s); }));
+  }
   st = hip_status(timed_launch("decode_attn", s, [&] { return launch_decode(a, s); }));
   if (st != SPA_OK) return st;
   return hip_status(timed_launch("combine", s, [&] { return launch_combine(a, s); }));

@@ -83,13 +83,17 @@ __device__ void decode_unit_range(const FwdArgs& a, int u, int rb, int64_t nt, i
   const int qpos = L - nq + qi;   // last visible position of this row (causal)
   if (rb * 16 >= rows) return;    // row block without rows (shorter chunk)
 
+  // Q operand of the row block (16 rows x D); rows past the chunk read row 0 and are zeroed
   s16x8 qreg[KB];
   {
-    const __bf16* qp = a.q + ((int64_t)(q0 + (row_ok ? qi : 0)) * a.Hq + g * G + hh) * D;
+    const int qrow = row_ok ? qi : 0;
+    const int qh = row_ok ? hh : 0;
+    const __bf16* qp = a.q + ((int64_t)(q0 + qrow) * a.Hq + g * G + qh) * D + grp * 8;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      s16x8 z = {0, 0, 0, 0, 0, 0, 0, 0};
-      qreg[kb] = row_ok ? *reinterpret_cast<const s16x8*>(qp + kb * 32 + grp * 8) : z;
+      const s16x8 v = *reinterpret_cast<const s16x8*>(qp + kb * 32);
+      const s16x8 z = {0, 0, 0, 0, 0, 0, 0, 0};
+      qreg[kb] = row_ok ? v : z;
     }
   }
 
@@ -98,34 +102,6 @@ __device__ void decode_unit_range(const FwdArgs& a, int u, int rb, int64_t nt, i
   const int voff = j * kTile * 2 + grp * 8;
   const int tpp_log2 = a.tpp_log2;
   const int tpp_mask = (1 << tpp_log2) - 1;
-
-  // physical pages of up to 64 consecutive entries, one per lane
-  int64_t batch_e0 = -(1ll << 40);
-  int b_jpg = -1, b_ph = -1;
-  auto page_of = [&](int64_t loc, int& jpg, int& ph) {
-    const int64_t e = (int64_t)e_unit0 + (loc >> tpp_log2);
-    if (e < batch_e0 || e >= batch_e0 + kWave) {
-      batch_e0 = e;
-      const int64_t me = e + lane;
-      int jp = -1, pp = -1;
-      if (me < e_unit1) {
-        jp = a.sel_pages[me];
-        if (jp >= 0 && jp < npg)
-          pp = translate_page(seg_row, a.page_table, jp, a.pps, a.max_segs, a.n_virtual, a.n_phys);
-      }
-      b_jpg = jp;
-      b_ph = pp;
-    }
-    const int idx = (int)(e - batch_e0);
-    jpg = __builtin_amdgcn_readlane(b_jpg, idx);
-    ph = __builtin_amdgcn_readlane(b_ph, idx);
-  };
-  auto tile_ptrs = [&](int ph, int sub, const __bf16*& kt, const __bf16*& vt) {
-    // an unusable page reads physical page 0 and is fully masked
-    const int64_t base = ((int64_t)(ph < 0 ? 0 : ph) * P + sub * kTile) * D;
-    kt = a.k_pool + base;
-    vt = a.v_pool + base;
-  };
 
   float m = -INFINITY;
   float lsum = 0.f;
@@ -139,15 +115,11 @@ __device__ void decode_unit_range(const FwdArgs& a, int u, int rb, int64_t nt, i
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) s = mfma16x16x32(tile.k[kb], qreg[kb], s);
     // this lane holds row j, tokens 4*grp + 0..3 of the tile
-    const bool page_ok = ph >= 0;
+    const int lim = ph >= 0 ? min(L - 1, qpos) : -1;   // last visible position
     const int tok0 = jpg * P + sub * kTile + grp * 4;
     float sv[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int tp = tok0 + e;
-      const bool ok = page_ok && tp < L && tp <= qpos;
-      sv[e] = ok ? s[e] * a.scale_log2 : -INFINITY;
-    }
+    for (int e = 0; e < 4; ++e) sv[e] = tok0 + e <= lim ? s[e] * a.scale_log2 : -INFINITY;
     float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -167,24 +139,50 @@ __device__ void decode_unit_range(const FwdArgs& a, int u, int rb, int64_t nt, i
       acc[nb] = mfma16x16x16(tile.v[nb], pb, acc[nb]);
     }
   };
-  auto fetch = [&](KvTile<D>& tile, int64_t loc, int& jpg, int& ph, int& sub) {
-    page_of(loc, jpg, ph);
-    sub = (int)(loc & tpp_mask);
-    const __bf16 *kt, *vt;
-    tile_ptrs(ph, sub, kt, vt);
-    load_kv_tile<D>(tile, kt, vt, koff, voff);
-  };
 
-  // two tile buffers in flight: load t+1 while computing t
-  KvTile<D> ta_buf, tb_buf;
-  int x_jpg, x_ph, x_sub, y_jpg = -1, y_ph = -1, y_sub = 0;
-  fetch(ta_buf, la, x_jpg, x_ph, x_sub);
-  for (int64_t t = la; t < lb; t += 2) {
-    if (t + 1 < lb) fetch(tb_buf, t + 1, y_jpg, y_ph, y_sub);
-    step(ta_buf, x_jpg, x_ph, x_sub);
-    if (t + 1 >= lb) break;
-    if (t + 2 < lb) fetch(ta_buf, t + 2, x_jpg, x_ph, x_sub);
-    step(tb_buf, y_jpg, y_ph, y_sub);
+  // Pages are translated 64 at a time (one per lane: selected id ->
+  // segment -> virtual -> physical); tiles then stream through two register
+  // buffers, loading tile t+1 while tile t is computed.
+  const int64_t e_first = la >> tpp_log2;
+  const int64_t e_last = (lb - 1) >> tpp_log2;
+  for (int64_t eb = e_first; eb <= e_last; eb += kWave) {
+    int b_jpg = -1, b_ph = -1;
+    if (eb + lane <= e_last) {
+      b_jpg = a.sel_pages[e_unit0 + eb + lane];
+      if (b_jpg >= 0 && b_jpg < npg)
+        b_ph = translate_page(seg_row, a.page_table, b_jpg, a.pps, a.max_segs, a.n_virtual, a.n_phys);
+      else
+        b_jpg = -1;
+    }
+    const int64_t t0 = max(la, eb << tpp_log2);
+    const int64_t t1 = min(lb, (eb + kWave) << tpp_log2);
+    auto fetch = [&](KvTile<D>& tile, int64_t t, int& jpg, int& ph, int& sub) {
+      const int idx = (int)((t >> tpp_log2) - eb);
+      jpg = __builtin_amdgcn_readlane(b_jpg, idx);
+      ph = __builtin_amdgcn_readlane(b_ph, idx);
+      sub = (int)(t & tpp_mask);
+      // an unusable page reads physical page 0 and is fully masked
+      const int64_t base = uniform64(((int64_t)(ph < 0 ? 0 : ph) * P + sub * kTile) * D);
+      load_kv_tile<D>(tile, a.k_pool + base, a.v_pool + base, koff, voff);
+    };
+    // Loads are issued unconditionally (past the end they re-read the last
+    // tile, already in cache) so that every compute step waits only for its
+    // own buffer while the other buffer's loads stay in flight.
+    KvTile<D> ta_buf, tb_buf;
+    int x_jpg, x_ph, x_sub, y_jpg, y_ph, y_sub;
+    // The scheduling barriers keep each buffer's loads ahead of the other
+    // buffer's compute (the scheduler would otherwise sink them to their use).
+    fetch(ta_buf, t0, x_jpg, x_ph, x_sub);
+    for (int64_t t = t0; t < t1; t += 2) {
+      fetch(tb_buf, min(t + 1, t1 - 1), y_jpg, y_ph, y_sub);
+      __builtin_amdgcn_sched_barrier(0);
+      step(ta_buf, x_jpg, x_ph, x_sub);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(ta_buf, min(t + 2, t1 - 1), x_jpg, x_ph, x_sub);
+      __builtin_amdgcn_sched_barrier(0);
+      if (t + 1 < t1) step(tb_buf, y_jpg, y_ph, y_sub);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 
   // row totals: the four lane groups hold disjoint token subsets

@@ -34,7 +34,7 @@ struct FwdArgs {
   int32_t tpp_log2;           // log2(P / 16)
   int32_t pps, max_segs, units, max_q_len, total_q;
   int32_t total_waves;        // decode: waves of the split-KV launch
-  int32_t row_blocks;         // query-row blocks of 16 per unit: ceil(max_q_len * G / 16)
+  int32_t row_blocks;         // query-row blocks per unit: ceil(max_q_len * G / rows per block)
   float scale_log2;           // softmax scale * log2(e)
 };
 
@@ -84,6 +84,10 @@ constexpr int kSelectKeyCache = 4096;  // keys held in LDS by the select kernel
 hipError_t launch_decode(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_combine(const FwdArgs& a, hipStream_t stream);
 int decode_blocks_per_cu(int D, int units);
+
+hipError_t launch_prefill(const FwdArgs& a, hipStream_t stream);
+int prefill_rows_per_block();
+constexpr int kPrefillMinRows = 128;   // n_q * G at or above this runs the prefill kernel
 
 hipError_t launch_select_scores(const SelArgs& a, hipStream_t stream);
 hipError_t launch_select_fill(const SelArgs& a, hipStream_t stream);

@@ -84,6 +84,18 @@ EDGE = {
                            shared_prefix_segments=1),
     "spare_phys_pages": dict(extra_phys_pages=37),
     "scaled_keys": dict(k_page_scale_sigma=0.5, sel_mode=I.SEL_RANDOM_HASH, budgets=[20, 10]),
+    # chunks of >= 128 query rows per unit run the matrix-core prefill kernel
+    "prefill_g4": dict(q_lens=[40, 33], ctx_lens=[700, 333]),
+    "prefill_d64_p32": dict(D=64, P=32, seg_tokens=256, q_lens=[64, 70], ctx_lens=[400, 300]),
+    "prefill_mha": dict(Hq=2, Hkv=2, q_lens=[130, 200], ctx_lens=[400, 200]),
+    "prefill_random_empty": dict(sel_mode=I.SEL_RANDOM_HASH, budgets=[0, 3], q_lens=[50, 40],
+                                 ctx_lens=[500, 300], sel_seed=21),
+    "prefill_forced_tail": dict(sel_mode=I.SEL_RANDOM_HASH, budgets=[12, 9], forced_tail=3,
+                                q_lens=[45, 38], ctx_lens=[1500, 800], sel_seed=22),
+    "prefill_head_class": dict(sel_mode=I.SEL_HEAD_CLASS, head_policy=[0, 1], n_sink=8, window=64,
+                               q_lens=[40, 40], ctx_lens=[900, 300]),
+    "prefill_rows_g16": dict(Hq=32, Hkv=2, q_lens=[33, 17], ctx_lens=[600, 256]),
+    "prefill_many_entries": dict(ctx_lens=[20000, 3000], q_lens=[40, 8], seg_tokens=4096),
 }
 
 
