@@ -39,7 +39,9 @@ def common_flags() -> list[str]:
 # per-source extra flags: matrix-core accumulators in ordinary VGPRs (the
 # decode kernel rescales them every tile; AGPR accumulators cost a copy each way)
 EXTRA = {"decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-         "prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+         # no NaN operands reach the prefill arithmetic (masked keys are -inf
+         # by selection, stale slots are zeroed), so max needs no quieting
+         "prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"]}
 
 
 def _compile(src: str) -> str:

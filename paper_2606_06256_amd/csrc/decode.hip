@@ -42,12 +42,12 @@ struct KvTile {
 // One 16-token tile through buffer descriptors (wave-uniform base in SGPRs).
 // Lane (j, grp) takes: K chunk (kb * 4 + grp) of token j (16 B at
 // koff + kb * 1024), and V dims nb * 16 + j for tokens 4 * grp .. 4 * grp + 3
-// (8 B at voff + nb * 512).
+// (8 B at voff + nb * 512). range = 0 makes every load return zeros.
 template <int D>
 __device__ __forceinline__ void load_kv_tile(KvTile<D>& t, const __bf16* kt, const __bf16* vt,
-                                             int koff, int voff) {
-  const __amdgpu_buffer_rsrc_t kr = make_rsrc(kt, kTile * D * 2);
-  const __amdgpu_buffer_rsrc_t vr = make_rsrc(vt, kTile * D * 2);
+                                             int koff, int voff, int range) {
+  const __amdgpu_buffer_rsrc_t kr = make_rsrc(kt, range);
+  const __amdgpu_buffer_rsrc_t vr = make_rsrc(vt, range);
 #pragma unroll
   for (int kb = 0; kb < D / 32; ++kb)
     t.k[kb] = __builtin_bit_cast(s16x8, __builtin_amdgcn_raw_buffer_load_b128(kr, koff, kb * 1024, 0));
@@ -161,9 +161,19 @@ __device__ void decode_unit_range(const FwdArgs& a, int u, int rb, int64_t nt, i
       jpg = __builtin_amdgcn_readlane(b_jpg, idx);
       ph = __builtin_amdgcn_readlane(b_ph, idx);
       sub = (int)(t & tpp_mask);
-      // an unusable page reads physical page 0 and is fully masked
+      // an unusable page reads as zeros; so do V slots past the context (their
+      // probability is 0, and stale contents there must not reach the sum)
       const int64_t base = uniform64(((int64_t)(ph < 0 ? 0 : ph) * P + sub * kTile) * D);
-      load_kv_tile<D>(tile, a.k_pool + base, a.v_pool + base, koff, voff);
+      load_kv_tile<D>(tile, a.k_pool + base, a.v_pool + base, koff, voff,
+                      ph >= 0 ? kTile * D * 2 : 0);
+      const int valid = L - (jpg * P + sub * kTile);   // tokens of the tile inside the context
+      if (ph >= 0 && valid < kTile) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (grp * 4 + e >= valid) tile.v[nb][e] = 0;
+      }
     };
     // Loads are issued unconditionally (past the end they re-read the last
     // tile, already in cache) so that every compute step waits only for its

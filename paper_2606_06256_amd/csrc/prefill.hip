@@ -45,7 +45,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
   constexpr int KS = D / 16;               // QK steps (16 dims each)
   constexpr int NDB = D / 32;              // 32-dim blocks of the output
   constexpr int TB = kTile * D * 2;        // bytes per tile
-  __shared__ __attribute__((aligned(16))) char s_kv[2][4 * TB];   // stage: K0 K1 V0 V1
+  __shared__ __attribute__((aligned(16))) char s_kv[3][4 * TB];   // stage: K0 K1 V0 V1
   __shared__ int s_pos[kPfEntries];        // first token position of each entry's page, -1 unusable
   __shared__ int s_phys[kPfEntries];
 
@@ -129,7 +129,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
     const int nt = cn << tpp_log2;         // tiles in this chunk
     const int nsteps = (nt + 1) >> 1;
     // cooperative copy: thread t moves 16 B of K and 16 B of V of tile (t / 256)
-    const int ct = tid >> 8;               // which tile of the step
+    const int ct = __builtin_amdgcn_readfirstlane(tid >> 8);   // tile of the step (per wave)
     const int cb = (tid & 255) * 16;       // byte offset inside the tile (D = 128)
     auto tile_info = [&](int t, int& ph, int& pos) {
       if (t >= nt) { ph = -1; pos = -1; return; }
@@ -137,81 +137,140 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       ph = s_phys[e];
       pos = s_pos[e] < 0 ? -1 : s_pos[e] + (t & (tpp - 1)) * kTile;
     };
+    // unusable tiles and bytes past the tile read as zeros (zero-range descriptor)
     auto load_step = [&](int st, s16x8& kx, s16x8& vx) {
       int ph, pos;
       tile_info(2 * st + ct, ph, pos);
-      const s16x8 z = {0, 0, 0, 0, 0, 0, 0, 0};
-      kx = z;
-      vx = z;
-      if (ph >= 0 && cb < TB) {
-        const int64_t base = ((int64_t)ph * P + (int64_t)((2 * st + ct) & (tpp - 1)) * kTile) * D;
-        kx = *reinterpret_cast<const s16x8*>(reinterpret_cast<const char*>(a.k_pool + base) + cb);
-        vx = *reinterpret_cast<const s16x8*>(reinterpret_cast<const char*>(a.v_pool + base) + cb);
-      }
+      ph = __builtin_amdgcn_readfirstlane(ph);        // wave-uniform: ct is per wave
+      const int64_t base =
+          uniform64(((int64_t)(ph < 0 ? 0 : ph) * P + (int64_t)((2 * st + ct) & (tpp - 1)) * kTile) * D);
+      const int range = ph >= 0 ? TB : 0;
+      kx = __builtin_bit_cast(s16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                                         make_rsrc(a.k_pool + base, range), cb, 0, 0));
+      vx = __builtin_bit_cast(s16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                                         make_rsrc(a.v_pool + base, range), cb, 0, 0));
     };
-    auto store_stage = [&](int stage, const s16x8& kx, const s16x8& vx) {
+    // V slots past the context are stored as zeros (their probability is 0,
+    // and stale contents there must not reach the sum); 16 B = tokens
+    // tok0 .. tok0 + 7 of one dimension
+    auto store_stage = [&](int st, int stage, const s16x8& kx, s16x8 vx) {
+      int ph, pos;
+      tile_info(2 * st + ct, ph, pos);
+      const int tok0 = (cb & 31) >> 1;
+      const int valid = L - pos;
+      if (ph >= 0 && valid < tok0 + 8) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (tok0 + e >= valid) vx[e] = 0;
+      }
       if (cb < TB) {
         *reinterpret_cast<s16x8*>(&s_kv[stage][ct * TB + cb]) = kx;
-        *reinterpret_cast<s16x8*>(&s_kv[stage][2 * TB + ct * TB + cb]) = vx;
+        // V row d (16 tokens) is stored in the operand's key order: half h
+        // holds tokens 4h..4h+3 and 8+4h..8+4h+3, and sits at half
+        // h ^ ((d >> 3) & 1) so that one 16-byte operand read of 32 rows hits
+        // distinct LDS banks. This thread holds tokens 8q..8q+7 of row d.
+        const int d = cb >> 5;
+        const int q = (cb >> 4) & 1;
+        const int sw = (d >> 3) & 1;
+        char* row = &s_kv[stage][2 * TB + ct * TB + d * 32];
+        const s16x4 lo = {vx[0], vx[1], vx[2], vx[3]};   // tokens 8q + 0..3 -> half 0
+        const s16x4 hi = {vx[4], vx[5], vx[6], vx[7]};   // tokens 8q + 4..7 -> half 1
+        *reinterpret_cast<s16x4*>(row + ((0 ^ sw) * 16) + q * 8) = lo;
+        *reinterpret_cast<s16x4*>(row + ((1 ^ sw) * 16) + q * 8) = hi;
       }
     };
 
-    s16x8 kx, vx;
-    load_step(0, kx, vx);
-    store_stage(0, kx, vx);
-    __syncthreads();
-    for (int st = 0; st < nsteps; ++st) {
-      const int stage = st & 1;
-      int ph0, pos0, ph1, pos1;
-      tile_info(2 * st, ph0, pos0);
-      tile_info(2 * st + 1, ph1, pos1);
-      if (pos0 > vis_hi || (pos0 < 0 && pos1 > vis_hi)) { done = true; break; }   // block-uniform
-      const bool has_next = st + 1 < nsteps;
-      if (has_next) load_step(st + 1, kx, vx);
-
-      // S^T = K . Q^T
+    // Pipeline. LDS holds three key steps: the step being finished (its V),
+    // the next step (its K, for the next scores) and the step being copied in.
+    // Global loads run three steps ahead through three register sets. Within
+    // a step the exponentials of step st are interleaved with the score
+    // products of step st + 1, so the vector unit and the matrix cores work
+    // at the same time; then P.V of step st runs and the barrier closes it.
+    auto qk = [&](int stage) -> f32x16 {
       const char* kb = s_kv[stage];
       f32x16 sacc = {};
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
+      for (int s2 = 0; s2 < KS; ++s2) {
         const s16x8 kop = *reinterpret_cast<const s16x8*>(
-            kb + (j >> 4) * TB + (((2 * s + hf) * kTile + (j & 15)) * 16));
-        sacc = mfma32x32x16(kop, qreg[s], sacc);
+            kb + (j >> 4) * TB + (((2 * s2 + hf) * kTile + (j & 15)) * 16));
+        sacc = mfma32x32x16(kop, qreg[s2], sacc);
       }
-      // lane's keys: kk(rr) = 8 * (rr / 4) + 4 * hf + rr % 4 (tile kk / 16)
+      return sacc;
+    };
+    s16x8 kx0, vx0, kx1, vx1, kx2, vx2;
+    load_step(0, kx0, vx0);
+    load_step(1, kx1, vx1);
+    load_step(2, kx2, vx2);
+    store_stage(0, 0, kx0, vx0);
+    store_stage(1, 1, kx1, vx1);
+    __syncthreads();
+    f32x16 sa = qk(0), sb = {};
+
+    // one step; sc = stage of st, sn = stage of st + 1, sw = stage for st + 2;
+    // cur holds the scores of st, nxt receives those of st + 1.
+    // Returns false once every later key is past the block's last query.
+    auto body = [&](int st, int sc, int sn, int sw, s16x8& kl, s16x8& vl, const s16x8& ks,
+                    const s16x8& vs, f32x16& cur, f32x16& nxt) -> bool {
+      int ph0, pos0, ph1, pos1;
+      tile_info(2 * st, ph0, pos0);
+      tile_info(2 * st + 1, ph1, pos1);
+      if (pos0 > vis_hi || (pos0 < 0 && pos1 > vis_hi)) return false;   // block-uniform
+      load_step(st + 3, kl, vl);           // this set's data (step st) is already in LDS
+      f32x16& sv = cur;
+
+      // lane's keys: kk(rr) = 8 * (rr / 4) + 4 * hf + rr % 4 (tile kk / 16);
+      // masked in place (no copy on the common, fully visible path)
       const bool full = ph0 >= 0 && ph1 >= 0 && pos1 + kTile - 1 <= vis_lo;
-      float sv[16];
-      if (full) {
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) sv[rr] = sacc[rr];
-      } else {
-        const int lim = vis_row;
+      if (!full) {
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
           const int kk = 8 * (rr >> 2) + 4 * hf + (rr & 3);
           const int tp = (kk < 16 ? pos0 : pos1);
-          const int p = tp + (kk & 15);
-          sv[rr] = (tp >= 0 && p <= lim) ? sacc[rr] : -INFINITY;
+          if (!(tp >= 0 && tp + (kk & 15) <= vis_row)) sv[rr] = -INFINITY;
         }
       }
-      float mx = sv[0];
+      float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
 #pragma unroll
-      for (int rr = 1; rr < 16; ++rr) mx = fmaxf(mx, sv[rr]);
+      for (int rr = 4; rr < 16; rr += 2) mx = fmaxf(mx, fmaxf(sv[rr], sv[rr + 1]));
       mx = fmaxf(mx, swap_halves(mx));
+      // The reference max m moves only when a row's max exceeds it by more
+      // than 2^8 in probability (the result is unchanged: numerator and sum
+      // share the reference; probabilities stay <= 256, far inside bf16/fp32).
       const float m_new = fmaxf(m, mx);
-      if (__ballot(m_new > m) != 0ull) {   // rescale only when some row's max grew
-        const float alpha = (m == -INFINITY) ? 0.f : fast_exp2((m - m_new) * c);
+      const bool grow = m == -INFINITY ? m_new > m : (m_new - m) * c > 8.f;
+      if (__ballot(grow) != 0ull) {
+        const float mt = grow ? m_new : m;
+        const float alpha = (m == -INFINITY) ? 0.f : fast_exp2((m - mt) * c);
         lsum *= alpha;
 #pragma unroll
         for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
-        m = m_new;
+        m = mt;
       }
       const float mc = (m == -INFINITY) ? 0.f : m * c;
+
+      // exponentials of step st, interleaved with the scores of step st + 1
       float pv[16];
+      {
+        const char* kb = s_kv[sn];
+        f32x16 sn_acc = {};
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        pv[rr] = fast_exp2(fmaf(sv[rr], c, -mc));
-        lsum += pv[rr];
+        for (int s2 = 0; s2 < KS; ++s2) {
+          const s16x8 kop = *reinterpret_cast<const s16x8*>(
+              kb + (j >> 4) * TB + (((2 * s2 + hf) * kTile + (j & 15)) * 16));
+          sn_acc = mfma32x32x16(kop, qreg[s2], sn_acc);
+#pragma unroll
+          for (int e = 0; e < 16 / KS; ++e) {
+            const int rr = s2 * (16 / KS) + e;
+            pv[rr] = fast_exp2(fmaf(sv[rr], c, -mc));
+          }
+        }
+        nxt = sn_acc;
+      }
+      {
+        float t8[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) t8[i] = pv[i] + pv[i + 8];
+        lsum += ((t8[0] + t8[4]) + (t8[1] + t8[5])) + ((t8[2] + t8[6]) + (t8[3] + t8[7]));
       }
       s16x8 pb[2];
 #pragma unroll
@@ -221,22 +280,34 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
         pb[t] = (s16x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       }
       // O^T += V^T . P^T; k-slot 8 hf + e of step t <-> key 16 t + (e < 4 ? 4 hf + e : 8 + 4 hf + e - 4)
-      const char* vb = s_kv[stage] + 2 * TB;
+      const char* vb = s_kv[sc] + 2 * TB;
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
 #pragma unroll
         for (int d = 0; d < NDB; ++d) {
           const int dd = d * 32 + j;
-          const char* row = vb + t * TB + dd * kTile * 2;
-          const s16x4 v0 = *reinterpret_cast<const s16x4*>(row + 8 * hf);
-          const s16x4 v1 = *reinterpret_cast<const s16x4*>(row + 16 + 8 * hf);
-          const s16x8 vop = (s16x8){v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+          const s16x8 vop = *reinterpret_cast<const s16x8*>(
+              vb + t * TB + dd * kTile * 2 + (hf ^ ((dd >> 3) & 1)) * 16);
           acc[d] = mfma32x32x16(vop, pb[t], acc[d]);
         }
       }
-
-      if (has_next) store_stage(stage ^ 1, kx, vx);
+      if (st + 2 < nsteps) store_stage(st + 2, sw, ks, vs);
       __syncthreads();
+      return true;
+    };
+    // set and stage of step x: x % 3; score buffer of step x: x % 2
+    for (int st = 0; st < nsteps; st += 6) {
+      if (!body(st, 0, 1, 2, kx0, vx0, kx2, vx2, sa, sb)) { done = true; break; }
+      if (st + 1 >= nsteps) break;
+      if (!body(st + 1, 1, 2, 0, kx1, vx1, kx0, vx0, sb, sa)) { done = true; break; }
+      if (st + 2 >= nsteps) break;
+      if (!body(st + 2, 2, 0, 1, kx2, vx2, kx1, vx1, sa, sb)) { done = true; break; }
+      if (st + 3 >= nsteps) break;
+      if (!body(st + 3, 0, 1, 2, kx0, vx0, kx2, vx2, sb, sa)) { done = true; break; }
+      if (st + 4 >= nsteps) break;
+      if (!body(st + 4, 1, 2, 0, kx1, vx1, kx0, vx0, sa, sb)) { done = true; break; }
+      if (st + 5 >= nsteps) break;
+      if (!body(st + 5, 2, 0, 1, kx2, vx2, kx1, vx1, sb, sa)) { done = true; break; }
     }
   }
 

@@ -181,6 +181,37 @@ def test_physical_placement_invariance():
     assert torch.equal(a.out, b.out) and torch.equal(a.lse, b.lse)
 
 
+@pytest.mark.parametrize("q_lens", [[1, 1], [40, 33]])
+def test_stale_slots_never_reach_the_result(q_lens):
+    """Slots past the context in a page and unused pages may hold anything (here
+    NaN): they never enter the softmax, so results are bitwise unchanged."""
+    _require_gpu()
+    wl = I.build(_spec(name="stale", P=32, ctx_lens=[701, 333], q_lens=q_lens, extra_phys_pages=9))
+    clean = DeviceWorkload(wl)
+    clean.step()
+    dirty = DeviceWorkload(wl)
+    nan = torch.tensor(float("nan"), dtype=torch.bfloat16, device="cuda")
+    used = torch.zeros(wl.num_phys, dtype=torch.bool)
+    for r in range(wl.B):
+        L = int(wl.ctx_lens[r])
+        for g in range(wl.Hkv):
+            ph = wl.unit_phys_pages(r, g)
+            used[torch.from_numpy(ph.astype(np.int64))] = True
+            last = int(ph[-1])
+            valid = L - (len(ph) - 1) * wl.P
+            kt = dirty.k_pool[last].view(wl.P // 16, wl.D // 8, 16, 8)
+            vt = dirty.v_pool[last].view(wl.P // 16, wl.D, 16)
+            for t in range(valid, wl.P):
+                kt[t // 16, :, t % 16, :] = nan
+                vt[t // 16, :, t % 16] = nan
+    dirty.k_pool[~used.cuda()] = nan
+    dirty.v_pool[~used.cuda()] = nan
+    dirty.step()
+    torch.cuda.synchronize()
+    assert torch.equal(clean.out, dirty.out) and torch.equal(clean.lse, dirty.lse)
+    assert torch.isfinite(dirty.out.float()).all()
+
+
 def test_page_summary_bit_exact():
     _require_gpu()
     from oracle import segpa_oracle as O
