@@ -56,6 +56,14 @@ __device__ __forceinline__ void load_kv_tile(KvTile<D>& t, const __bf16* kt, con
     t.v[nb] = __builtin_bit_cast(s16x4, __builtin_amdgcn_raw_buffer_load_b64(vr, voff, nb * 512, 0));
 }
 
+// Tiles per wave share: an equal split of all T virtual tiles over the waves,
+// but at least kMinChunk tiles so that small problems are not cut into many
+// tiny partials (waves past the end get no work).
+constexpr int64_t kMinChunk = 8;
+__device__ __forceinline__ int64_t stream_chunk(int64_t T, int waves) {
+  return max((T + waves - 1) / waves, kMinChunk);
+}
+
 // One wave processes unit-local tiles [la, lb) of unit u (nt tiles) for row
 // block rb.
 template <int D>
@@ -233,7 +241,7 @@ __global__ __launch_bounds__(kDecodeBlock) void decode_attn_kernel(const FwdArgs
   const int RB = a.row_blocks;
   const int wave = blockIdx.x * (kDecodeBlock / kWave) + (threadIdx.x >> 6);
   const int64_t T = ((int64_t)s_indptr[U] << a.tpp_log2) * RB;   // virtual tiles
-  const int64_t chunk = (T + a.total_waves - 1) / a.total_waves;
+  const int64_t chunk = stream_chunk(T, a.total_waves);
   const int64_t t_begin = (int64_t)wave * chunk;
   const int64_t t_end = min(T, t_begin + chunk);
   if (t_begin >= t_end) return;
@@ -268,9 +276,14 @@ __global__ __launch_bounds__(kDecodeBlock) void decode_attn_kernel(const FwdArgs
 
 // Merge the split partials of every virtual unit (unit, row block) that spans
 // several waves; write O = 0, LSE = -inf for units without selected tiles.
-// One block per virtual unit.
+// One block per virtual unit. All partial loads of a phase are independent
+// (no load waits for the previous one): the per-row max and sum come from a
+// block reduction, then every output element sums its partials.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(const FwdArgs a) {
+  constexpr int kRows = 16;
+  constexpr int kLanesPerRow = 256 / kRows;     // 16 threads per row in the reductions
+  constexpr int kCacheW = 64;                   // partial LSEs kept in LDS
   const int RB = a.row_blocks;
   const int v = blockIdx.x;
   const int u = v / RB;
@@ -288,55 +301,83 @@ __global__ __launch_bounds__(256) void combine_kernel(const FwdArgs a) {
   const int G = a.G;
   const int q0 = clampv(a.q_indptr[r], 0, a.total_q);
   const int nq = clampv(a.q_indptr[r + 1] - q0, 0, min(a.max_q_len, a.total_q - q0));
-  const int row0 = rb * 16;
-  const int rows = min(16, nq * G - row0);
+  const int row0 = rb * kRows;
+  const int rows = min(kRows, nq * G - row0);
   if (rows <= 0) return;
 
   // must mirror the decode kernel's partition
   const bool empty = nt <= 0;
-  int64_t w0 = 0, w1 = 0;
+  int64_t w0 = 0, nw = 0;
   if (!empty) {
-    const int64_t chunk = (T + a.total_waves - 1) / a.total_waves;
+    const int64_t chunk = stream_chunk(T, a.total_waves);
     w0 = vt0 / chunk;
-    w1 = (vt0 + nt - 1) / chunk;
-    if (w0 == w1) return;   // one wave wrote the final output
+    nw = (vt0 + nt - 1) / chunk - w0 + 1;
+    if (nw == 1) return;   // one wave wrote the final output
   }
-  const int64_t sbase = (int64_t)u * RB + rb;
-  __shared__ float s_m[16], s_z[16];
+  const int64_t sbase = (int64_t)u * RB + rb + w0;   // slot of the first partial
+  __shared__ float s_lse[kCacheW][kRows];
+  __shared__ float s_red[kRows][kLanesPerRow];
+  __shared__ float s_m[kRows], s_z[kRows];
   const int tid = threadIdx.x;
-  if (!empty && tid < rows) {
+  const int row = tid % kRows;
+  const int lane_r = tid / kRows;
+
+  if (!empty) {
+    // row max over partials
     float M = -INFINITY;
-    for (int64_t w = w0; w <= w1; ++w) M = fmaxf(M, a.part_lse[(w + sbase) * 16 + tid]);
+    for (int64_t w = lane_r; w < nw; w += kLanesPerRow) {
+      const float x = a.part_lse[(sbase + w) * kRows + row];
+      if (w < kCacheW) s_lse[w][row] = x;
+      M = fmaxf(M, x);
+    }
+    s_red[row][lane_r] = M;
+    __syncthreads();
+    if (tid < kRows) {
+      float mm = -INFINITY;
+      for (int i = 0; i < kLanesPerRow; ++i) mm = fmaxf(mm, s_red[tid][i]);
+      s_m[tid] = mm;
+    }
+    __syncthreads();
+    const float Mr = s_m[row];
     float Z = 0.f;
-    if (M != -INFINITY)
-      for (int64_t w = w0; w <= w1; ++w) Z += fast_exp2(a.part_lse[(w + sbase) * 16 + tid] - M);
-    s_m[tid] = M;
-    s_z[tid] = Z;
+    if (Mr != -INFINITY)
+      for (int64_t w = lane_r; w < nw; w += kLanesPerRow) {
+        const float x = w < kCacheW ? s_lse[w][row] : a.part_lse[(sbase + w) * kRows + row];
+        Z += fast_exp2(x - Mr);
+      }
+    s_red[row][lane_r] = Z;
+    __syncthreads();
+    if (tid < kRows) {
+      float zz = 0.f;
+      for (int i = 0; i < kLanesPerRow; ++i) zz += s_red[tid][i];
+      s_z[tid] = zz;
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  for (int idx = tid; idx < rows * D; idx += blockDim.x) {
-    const int row = idx / D;
-    const int d = idx - row * D;
-    const int R = row0 + row;
+  // outputs: 4 consecutive dims per thread
+  for (int idx = tid; idx < rows * (D / 4); idx += blockDim.x) {
+    const int rr = idx / (D / 4);
+    const int d = (idx - rr * (D / 4)) * 4;
+    const int R = row0 + rr;
     const int qi = R / G;
     const int hh = R - qi * G;
     const int64_t orow = (int64_t)(q0 + qi) * a.Hq + g * G + hh;
-    float o = 0.f;
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
     float lse = -INFINITY;
-    if (!empty) {
-      const float M = s_m[row];
-      const float Z = s_z[row];
-      if (Z > 0.f) {
-        float acc = 0.f;
-        for (int64_t w = w0; w <= w1; ++w) {
-          const float wt = fast_exp2(a.part_lse[(w + sbase) * 16 + row] - M);
-          acc += wt * a.part_o[((w + sbase) * 16 + row) * D + d];
-        }
-        o = acc / Z;
-        lse = (M + __log2f(Z)) * kLn2;
+    if (!empty && s_z[rr] > 0.f) {
+      const float M = s_m[rr];
+      const float Z = s_z[rr];
+#pragma unroll 8
+      for (int64_t w = 0; w < nw; ++w) {
+        const float x = w < kCacheW ? s_lse[w][rr] : a.part_lse[(sbase + w) * kRows + rr];
+        const float wt = fast_exp2(x - M);
+        const f32x4 po = *reinterpret_cast<const f32x4*>(a.part_o + ((sbase + w) * kRows + rr) * D + d);
+        o += wt * po;
       }
+      o *= 1.f / Z;
+      lse = (M + __log2f(Z)) * kLn2;
     }
-    a.out[orow * D + d] = (__bf16)o;
+    *reinterpret_cast<s16x4*>(a.out + orow * D + d) = pack_bf16x4(o[0], o[1], o[2], o[3]);
     if (d == 0 && a.lse != nullptr) a.lse[orow] = lse;
   }
 }

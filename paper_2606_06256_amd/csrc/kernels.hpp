@@ -80,6 +80,7 @@ struct ValidateArgs {
 constexpr int kDecodeBlock = 256;   // 4 waves
 constexpr int kSelectBlock = 512;
 constexpr int kSelectKeyCache = 4096;  // keys held in LDS by the select kernel
+constexpr int kSelectCand = 1024;      // radix-select candidate list in LDS
 
 hipError_t launch_decode(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_combine(const FwdArgs& a, hipStream_t stream);

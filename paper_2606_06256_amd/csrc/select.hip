@@ -12,8 +12,10 @@
 // length, the query count and the parameters, so each block derives its CSR
 // offset by summing the counts of the units before it: no second launch and
 // no device-wide synchronisation. The ranked rules find the exact threshold
-// key by an 8-pass radix select (8-bit digits, LDS histogram) and then emit the
-// chosen pages in ascending order with block-wide prefix counts.
+// (key, page) pair by a radix select (LDS histograms; a 12-bit first digit,
+// then 8-bit digits over a shrinking candidate list, then an exact rank among
+// at most 128 candidates) and then emit the chosen pages in ascending order
+// with block-wide prefix counts.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -91,32 +93,29 @@ __device__ int64_t block_sum64(int64_t v, int64_t* scratch) {
   return t;
 }
 
-// Block-wide exclusive prefix counts of two predicates, in thread order, and
-// their block totals.
+// Block-wide exclusive prefix sum of one int per thread, in thread order, and
+// the block total.
 template <int BS>
-__device__ void block_scan2(bool x, bool y, int& ex_x, int& ex_y, int& tot_x, int& tot_y,
-                            int* scratch) {
-  const uint64_t bx = __ballot(x);
-  const uint64_t by = __ballot(y);
+__device__ void block_scan_int(int x, int& ex, int& tot, int* scratch) {
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  if (lane == 0) {
-    scratch[w] = __popcll(bx);
-    scratch[BS / 64 + w] = __popcll(by);
+  int incl = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
   }
+  if (lane == 63) scratch[w] = incl;
   __syncthreads();
-  int px = 0, py = 0;
-  tot_x = 0;
-  tot_y = 0;
+  int pre = 0;
+  tot = 0;
 #pragma unroll
   for (int i = 0; i < BS / 64; ++i) {
-    const int cx = scratch[i], cy = scratch[BS / 64 + i];
-    if (i < w) { px += cx; py += cy; }
-    tot_x += cx;
-    tot_y += cy;
+    const int c = scratch[i];
+    if (i < w) pre += c;
+    tot += c;
   }
-  ex_x = px + lane_prefix_count(bx);
-  ex_y = py + lane_prefix_count(by);
+  ex = pre + incl - x;
   __syncthreads();
 }
 
@@ -125,10 +124,13 @@ __device__ void block_scan2(bool x, bool y, int& ex_x, int& ex_y, int& tot_x, in
 __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs a) {
   constexpr int BS = kSelectBlock;
   __shared__ int64_t s_red[BS / 64];
-  __shared__ int s_scan[2 * (BS / 64)];
-  __shared__ uint32_t s_hist[256];
+  __shared__ int s_scan[BS / 64];
+  __shared__ uint32_t s_hist[4096];
   __shared__ uint64_t s_keys[kSelectKeyCache];
-  __shared__ int s_digit, s_need;
+  __shared__ uint64_t s_ck[kSelectCand], s_ck2[kSelectCand];
+  __shared__ int s_ci[kSelectCand], s_ci2[kSelectCand];
+  __shared__ int s_digit, s_need, s_count, s_fill, s_tidx;
+  __shared__ uint64_t s_tkey;
 
   const int u = blockIdx.x;
   const int tid = threadIdx.x;
@@ -153,7 +155,9 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
     return;
   }
 
-  // ranked rules: forced [0, a_end) U [b_begin, n); choose kk of [lo, hi)
+  // ranked rules: forced [0, a_end) U [b_begin, n); choose kk of [lo, hi).
+  // The choice is the kk smallest (key, page) pairs: find the kk-th smallest
+  // pair (T, pT) exactly, then keep every pair <= (T, pT).
   const int lo = I.a_end, hi = I.b_begin;
   const int nn = hi - lo;
   const int forced = lo + (n - hi);
@@ -164,78 +168,137 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
   auto key_of = [&](int p) -> uint64_t {
     return topk ? skeys[p] : random_key(sm_seed, r, g, p);
   };
-
   const bool take_all = kk >= nn;
   const bool take_none = kk <= 0;
   const bool cached = nn <= kSelectKeyCache;
   uint64_t T = 0;
-  int need = 0;
+  int pT = -1;
   if (!take_all && !take_none) {
     if (cached)
       for (int i = tid; i < nn; i += BS) s_keys[i] = key_of(lo + i);
+    __syncthreads();
+    auto key_at = [&](int i) -> uint64_t { return cached ? s_keys[i] : key_of(lo + i); };
+    // Radix passes narrow the candidates (keys that match `prefix` on the bits
+    // of `pmask`): the first pass over all keys with a 12-bit digit, the next
+    // ones with 8-bit digits, until at most kRankMax candidates remain or the
+    // whole key is fixed. Candidates go to an LDS list once they fit in it.
+    constexpr int kRankMax = 128;
     uint64_t prefix = 0, pmask = 0;
-    need = kk;
-    for (int shift = 56; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += BS) s_hist[i] = 0u;
+    int need = kk;                  // rank (1-based) of the threshold among candidates
+    int shift = 64;
+    int ncand = nn;
+    bool listed = false;            // candidates in s_ck/s_ci, else: filter [lo, hi)
+    while (ncand > kRankMax && shift > 0) {
+      const int bits = (shift == 64) ? 12 : 8;
+      const int nb = 1 << bits;
+      shift -= bits;
+      for (int i = tid; i < nb; i += BS) s_hist[i] = 0u;
+      if (tid == 0) s_fill = 0;
       __syncthreads();
-      for (int i = tid; i < nn; i += BS) {
-        const uint64_t k = cached ? s_keys[i] : key_of(lo + i);
-        if ((k & pmask) == prefix) atomicAdd(&s_hist[(k >> shift) & 255u], 1u);
+      const int len = listed ? ncand : nn;
+      for (int i = tid; i < len; i += BS) {
+        const uint64_t k = listed ? s_ck[i] : key_at(i);
+        if (listed || (k & pmask) == prefix)
+          atomicAdd(&s_hist[(uint32_t)(k >> shift) & (uint32_t)(nb - 1)], 1u);
       }
       __syncthreads();
-      if (tid < 64) {
-        const uint32_t h0 = s_hist[4 * tid], h1 = s_hist[4 * tid + 1];
-        const uint32_t h2 = s_hist[4 * tid + 2], h3 = s_hist[4 * tid + 3];
-        const int c = (int)(h0 + h1 + h2 + h3);
-        int incl = c;
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(incl, o);
-          if (tid >= o) incl += y;
-        }
-        const int excl = incl - c;
-        if (excl < need && need <= incl) {
-          int rem = need - excl;
-          int d = 4 * tid;
-          const uint32_t hs[4] = {h0, h1, h2, h3};
-          for (int q = 0; q < 4; ++q) {
-            if (rem <= (int)hs[q]) { d = 4 * tid + q; break; }
-            rem -= (int)hs[q];
+      // the bin that holds the need-th candidate: block-wide scan of bin groups
+      {
+        const int per = nb >= BS ? nb / BS : 1;
+        int c = 0;
+        if (tid * per < nb)
+          for (int q = 0; q < per; ++q) c += (int)s_hist[tid * per + q];
+        int ex, tot;
+        block_scan_int<BS>(c, ex, tot, s_scan);
+        if (c > 0 && ex < need && need <= ex + c) {
+          int rem = need - ex, d = tid * per;
+          for (int q = 0; q < per; ++q) {
+            const int h = (int)s_hist[tid * per + q];
+            if (rem <= h) { d = tid * per + q; break; }
+            rem -= h;
           }
           s_digit = d;
           s_need = rem;
+          s_count = (int)s_hist[d];
         }
       }
       __syncthreads();
-      prefix |= (uint64_t)s_digit << shift;
-      pmask |= 0xFFull << shift;
       need = s_need;
-      __syncthreads();
+      const int newc = s_count;
+      prefix |= (uint64_t)s_digit << shift;
+      pmask |= (uint64_t)(nb - 1) << shift;
+      if (newc <= kSelectCand) {
+        // unordered compaction of the survivors (order is irrelevant here)
+        for (int i = tid; i < len; i += BS) {
+          const uint64_t k = listed ? s_ck[i] : key_at(i);
+          if ((k & pmask) == prefix) {
+            const int slot = atomicAdd(&s_fill, 1);
+            s_ck2[slot] = k;
+            s_ci2[slot] = listed ? s_ci[i] : lo + i;
+          }
+        }
+        __syncthreads();
+        for (int i = tid; i < newc; i += BS) { s_ck[i] = s_ck2[i]; s_ci[i] = s_ci2[i]; }
+        __syncthreads();
+        listed = true;
+      }
+      ncand = newc;
     }
-    T = prefix;
+    if (shift == 0) {
+      // every candidate holds the key `prefix`: the threshold is the need-th
+      // lowest page index among them
+      if (tid == 0) { s_tkey = prefix; s_tidx = -1; }
+      int base = 0;
+      for (int c0 = 0; c0 < nn; c0 += BS) {
+        const int i = c0 + tid;
+        const bool m = i < nn && key_at(i) == prefix;
+        int ex, tot;
+        block_scan_int<BS>(m ? 1 : 0, ex, tot, s_scan);
+        if (m && base + ex == need - 1) s_tidx = lo + i;
+        base += tot;
+        if (base >= need) break;
+      }
+    } else {
+      if (!listed) {
+        // the loop did not run: nn <= kRankMax, every key is a candidate
+        for (int i = tid; i < nn; i += BS) { s_ck[i] = key_at(i); s_ci[i] = lo + i; }
+        __syncthreads();
+      }
+      // exact rank of each candidate pair (key, page) among the candidates
+      if (tid < ncand) {
+        const uint64_t k = s_ck[tid];
+        const int idx = s_ci[tid];
+        int rank = 0;
+        for (int i = 0; i < ncand; ++i) {
+          const uint64_t ko = s_ck[i];
+          rank += (ko < k || (ko == k && s_ci[i] < idx)) ? 1 : 0;
+        }
+        if (rank == need - 1) { s_tkey = k; s_tidx = idx; }
+      }
+    }
+    __syncthreads();
+    T = s_tkey;
+    pT = s_tidx;
   }
 
-  // ascending emission: forced pages, keys below T, and the first `need` keys equal to T
-  int out_base = 0, eq_base = 0;
+  // ascending emission: forced pages and the chosen pages
+  int out_base = 0;
   for (int c0 = 0; c0 < n; c0 += BS) {
     const int p = c0 + tid;
     const bool in = p < n;
     const bool nonforced = in && p >= lo && p < hi;
-    bool lt = false, eq = false;
-    if (nonforced && !take_all && !take_none) {
-      const uint64_t k = cached ? s_keys[p - lo] : key_of(p);
-      lt = k < T;
-      eq = k == T;
+    bool sel = in && !nonforced;
+    if (nonforced) {
+      if (take_all) sel = true;
+      else if (!take_none) {
+        const uint64_t k = cached ? s_keys[p - lo] : key_of(p);
+        sel = k < T || (k == T && p <= pT);
+      }
     }
-    int ex_eq, ex_sel, tot_eq, tot_sel;
-    // the equal-key rank must be known before the selection flag: two scans
-    int dummy_x, dummy_tx;
-    block_scan2<BS>(eq, false, ex_eq, dummy_x, tot_eq, dummy_tx, s_scan);
-    const bool chosen = take_all || lt || (eq && eq_base + ex_eq < need);
-    const bool sel = in && (!nonforced || (!take_none && chosen));
-    block_scan2<BS>(sel, false, ex_sel, dummy_x, tot_sel, dummy_tx, s_scan);
-    if (sel) out[out_base + ex_sel] = p;
-    out_base += tot_sel;
-    eq_base += tot_eq;
+    int ex, tot;
+    block_scan_int<BS>(sel ? 1 : 0, ex, tot, s_scan);
+    if (sel) out[out_base + ex] = p;
+    out_base += tot;
   }
 }
 
