@@ -18,6 +18,9 @@ python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N] [--no-cpu-bas
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -31,6 +34,102 @@ sys.path.insert(0, ROOT)
 METRIC = "attended KV tokens/s and achieved HBM GB/s (% of peak) for sparse decode"
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+# HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE passes, scaled by
+# what the same counters read for a device copy of known size. An entry counts
+# only while the kernel's sources hash to the recorded value.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+CSRC = os.path.join(ROOT, "paper_2606_06256_amd", "csrc")
+KERNELS = {  # bench name -> (kernel symbol fragment, sources that build it)
+    "decode_attn": ("decode_attn_kernel", ["common.hpp", "kernels.hpp", "decode.hip"]),
+    "prefill_attn": ("prefill_kernel", ["common.hpp", "kernels.hpp", "prefill.hip"]),
+}
+COPY_KERNEL = "copyBuffer"
+
+
+def kernel_sources_sha256(kname):
+    h = hashlib.sha256()
+    for f in KERNELS[kname][1]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(kname, workload):
+    """HBM bytes per launch of `kname` on `workload`, or None when no counter
+    entry exists or the kernel has changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            d = json.load(f)
+    except FileNotFoundError:
+        return None
+    e = d.get("kernels", {}).get(f"{kname}/{workload}")
+    if not e or e.get("sources_sha256") != kernel_sources_sha256(kname):
+        return None
+    return e["hbm_bytes_per_launch"]
+
+
+def pmc_mean_kib(out_dir, counter, fragment):
+    """Mean per-dispatch value of `counter` (KiB) over dispatches of kernels
+    whose name contains `fragment`, from a rocprofv3 --pmc csv output dir."""
+    per_dispatch = {}
+    for path in glob.glob(os.path.join(out_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if row.get("Counter_Name") != counter or fragment not in row.get("Kernel_Name", ""):
+                    continue
+                key = (path, row.get("Dispatch_Id"))
+                per_dispatch[key] = per_dispatch.get(key, 0.0) + float(row["Counter_Value"])
+    if not per_dispatch:
+        raise RuntimeError(f"no {counter} rows for '{fragment}' under {out_dir}")
+    return sum(per_dispatch.values()) / len(per_dispatch), len(per_dispatch)
+
+
+def pmc_command(bench_args):
+    """The counter runs behind an entry: one pass per counter, from /tmp on
+    the GPU host, with the repository root in $R."""
+    return ("cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc {FETCH_SIZE|WRITE_SIZE} "
+            "--kernel-include-regex 'decode_attn|prefill_kernel|copyBuffer' --output-format csv "
+            f"-d <out_dir> -o run -- python3 $R/bench.py {bench_args}")
+
+
+def write_traffic_entry(args):
+    """Record one kernel's HBM traffic from four rocprofv3 --pmc output dirs."""
+    from paper_2606_06256_amd import inputs as I
+    copy_bytes = 1 << 30
+    cf, _ = pmc_mean_kib(args.calib_fetch, "FETCH_SIZE", COPY_KERNEL)
+    cw, _ = pmc_mean_kib(args.calib_write, "WRITE_SIZE", COPY_KERNEL)
+    fetch_scale = copy_bytes / (cf * 1024)
+    write_scale = copy_bytes / (cw * 1024)
+    frag = KERNELS[args.kernel][0]
+    kf, nf = pmc_mean_kib(args.fetch, "FETCH_SIZE", frag)
+    kw, nw = pmc_mean_kib(args.write, "WRITE_SIZE", frag)
+    read_b = kf * 1024 * fetch_scale
+    write_b = kw * 1024 * write_scale
+    try:
+        with open(TRAFFIC_FILE) as f:
+            d = json.load(f)
+    except FileNotFoundError:
+        d = {"kernels": {}}
+    d["calibration"] = {"kernel": "__amd_rocclr_copyBuffer (torch device copy)",
+                        "bytes_read": copy_bytes, "bytes_written": copy_bytes,
+                        "FETCH_SIZE_kib": round(cf, 3), "WRITE_SIZE_kib": round(cw, 3),
+                        "fetch_scale": round(fetch_scale, 6), "write_scale": round(write_scale, 6),
+                        "command": pmc_command("--copy-calibration --steps 3")}
+    name = I.config(args.workload).spec.name
+    d["kernels"][f"{args.kernel}/{name}"] = {
+        "kernel": frag, "workload": name,
+        "FETCH_SIZE_kib": round(kf, 3), "WRITE_SIZE_kib": round(kw, 3), "dispatches": [nf, nw],
+        "hbm_read_bytes": int(read_b), "hbm_write_bytes": int(write_b),
+        "hbm_bytes_per_launch": int(read_b + write_b),
+        "sources_sha256": kernel_sources_sha256(args.kernel),
+        "command": pmc_command(f"--steps 5 --warmup 2 --no-cpu-baseline --workload {args.workload}"),
+    }
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(d, f, indent=1, sort_keys=True)
+        f.write("\n")
+    print(json.dumps(d["kernels"][f"{args.kernel}/{name}"]), flush=True)
 
 
 def algorithmic_bytes(wl, sel_indptr, sel_pages):
@@ -111,7 +210,18 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (scale for HBM byte counters)")
+    ap.add_argument("--record-traffic", choices=sorted(KERNELS),
+                    help="write the kernel's HBM traffic entry from rocprofv3 --pmc output dirs "
+                         "(--fetch, --write, --calib-fetch, --calib-write); runs nothing on the GPU")
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--calib-fetch")
+    ap.add_argument("--calib-write")
     args = ap.parse_args()
+    if args.record_traffic:
+        args.kernel = args.record_traffic
+        write_traffic_entry(args)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -186,19 +296,22 @@ def main():
     n_attn, ms_attn = prof[kname]
     attn_ms = ms_attn / n_attn
     achieved = abytes / (attn_ms * 1e-3) / 1e9
+    traffic = recorded_traffic(kname, wl.spec.name)
     if prefill:
         # the chunk's attention is a dense contraction: matrix-core bound
         flops = attention_flops(wl, ind, pages)
         tf = flops / (attn_ms * 1e-3) / 1e12
         roofline = {"kernel": kname, "bound": "mfma", "achieved": round(tf, 2),
                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                    "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
                     "flops_per_launch": flops, "launch_ms": round(attn_ms, 5),
                     "hbm_gbs": round(achieved, 1)}
     else:
         roofline = {"kernel": kname, "bound": "hbm", "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": None, "bytes_per_launch": abytes, "launch_ms": round(attn_ms, 5)}
+                    "traffic": traffic, "bytes_per_launch": abytes, "launch_ms": round(attn_ms, 5)}
+    if traffic is not None:
+        roofline["traffic_over_algorithmic_bytes"] = round(traffic / abytes, 4)
     kernels = {k: {"launches": n, "mean_ms": round(t / n, 5)} for k, (n, t) in prof.items()}
     line = {
         "metric": METRIC,
