@@ -10,8 +10,9 @@
 // One block per (unit, 256 query rows); 8 waves, 32 rows each (row = query *
 // G + head, so a GQA group shares its KV head). The unit's selected pages are
 // translated once per chunk of entries into LDS. Keys stream in steps of 32
-// (two 16-token tiles): the block copies the step's K and V tiles into one of
-// two LDS stages while the waves compute on the other. Per wave and step:
+// (two 16-token tiles): each thread loads its share of a step's K and V tiles
+// three steps ahead into registers and stores it into one of three LDS stages
+// while the waves compute on the others. Per wave and step:
 //   S^T[32 keys x 32 rows]  = K_step[32 x D] . Q^T       (D/16 steps, 32x32x16)
 //   O^T[D x 32 rows]       += V_step^T[D x 32] . P^T     (2 x D/32, 32x32x16)
 // In the S^T layout each lane holds 16 keys of one row, so the row max needs

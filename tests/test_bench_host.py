@@ -65,3 +65,11 @@ def test_traffic_entry_and_source_hash(tmp_path, monkeypatch):
     e["sources_sha256"] = "0" * 64
     json.dump(d, open(out, "w"))
     assert bench.recorded_traffic("decode_attn", "tiny") is None
+
+
+def test_code_text_ignores_comments_only():
+    a = "int x = 1;  // one\n/* block\n comment */ int y = 2;\n"
+    b = "int x = 1;\n// another note\nint y = 2;"
+    c = "int x = 1;\nint y = 3;"
+    assert bench._code_text(a) == bench._code_text(b)
+    assert bench._code_text(a) != bench._code_text(c)
