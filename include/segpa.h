@@ -99,7 +99,7 @@ typedef struct {
   int32_t total_q;            /* rows of q and out (= q_indptr[B]), >= 0 */
   int32_t reserved0;
   int64_t num_virtual_pages;  /* length of page_table */
-  int64_t num_phys_pages;     /* pages in each pool */
+  int64_t num_phys_pages;     /* pages in each pool; num_phys_pages * P / 16 < 2^28 */
   float softmax_scale;        /* <= 0 selects 1 / sqrt(D) */
 } spa_dims_t;
 

@@ -106,6 +106,8 @@ spa_status_t check_dims(const spa_dims_t* d) {
   if (units * max_pages >= (int64_t(1) << 31)) return SPA_ERR_UNSUPPORTED;
   if (d->num_phys_pages >= (int64_t(1) << 31) || d->num_virtual_pages >= (int64_t(1) << 31))
     return SPA_ERR_UNSUPPORTED;
+  // 16-token tiles of one pool are indexed in 28 bits (1 TiB of bf16 at D = 128)
+  if (d->num_phys_pages * (d->page_size / 16) >= (int64_t(1) << 28)) return SPA_ERR_UNSUPPORTED;
   if (d->num_q_heads > 4096 || (int64_t)d->total_q * d->num_q_heads >= (int64_t(1) << 31))
     return SPA_ERR_UNSUPPORTED;
   return SPA_OK;

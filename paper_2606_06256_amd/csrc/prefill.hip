@@ -9,16 +9,25 @@
 //
 // One block per (unit, 256 query rows); 8 waves, 32 rows each (row = query *
 // G + head, so a GQA group shares its KV head). The unit's selected pages are
-// translated once per chunk of entries into LDS. Keys stream in steps of 32
-// (two 16-token tiles): each thread loads its share of a step's K and V tiles
-// three steps ahead into registers and stores it into one of three LDS stages
-// while the waves compute on the others. Per wave and step:
+// translated once per chunk of entries into LDS, and every 32 key steps each
+// wave copies the next 64 steps' tile indices and flags into one register
+// (lane i <-> step i), read back with v_readlane, so no LDS round trip sits
+// in front of a step's loads. Keys stream in steps of 32 (two 16-token
+// tiles): each thread loads its share of a step's K and V tiles three steps
+// ahead into registers and stores it into one of four LDS stages. Per wave and
+// step:
 //   S^T[32 keys x 32 rows]  = K_step[32 x D] . Q^T       (D/16 steps, 32x32x16)
 //   O^T[D x 32 rows]       += V_step^T[D x 32] . P^T     (2 x D/32, 32x32x16)
 // In the S^T layout each lane holds 16 keys of one row, so the row max needs
 // one cross-half swap and the running max, the sum and the rescale are
 // lane-local; the 16 probabilities are, in order, the operand of the second
 // product (the key order inside a step is permuted identically for V).
+//
+// Waves w and w + 4 share a SIMD. Waves 4..7 run half a step behind: in the
+// interval between two barriers they first finish the previous step (its
+// P.V product), while waves 0..3 do the vector work of the current step, so
+// the matrix cores of each SIMD have one wave's products to run while the
+// other wave computes exponentials.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -30,7 +39,14 @@ __device__ __forceinline__ f32x16 mfma32x32x16(s16x8 a, s16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// value of lane l ^ 32 (v_permlane32_swap)
+// max of x over lanes l and l ^ 32 (v_permlane32_swap gives each lane's
+// partner value in one of its two results and its own in the other)
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// value of lane l ^ 32
 __device__ __forceinline__ float swap_halves(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(__lane_id() < 32 ? r[1] : r[0]);
@@ -40,13 +56,16 @@ constexpr int kPfWaves = 8;
 constexpr int kPfThreads = kPfWaves * 64;
 constexpr int kPfRows = kPfWaves * 32;     // query rows per block
 constexpr int kPfEntries = 1024;           // translated page entries held in LDS
+constexpr int kPfStages = 4;               // LDS key steps
+constexpr int kFlagStop = 1, kFlagFull = 2, kFlagPartial = 4;
 
 template <int D>
 __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a) {
   constexpr int KS = D / 16;               // QK steps (16 dims each)
   constexpr int NDB = D / 32;              // 32-dim blocks of the output
   constexpr int TB = kTile * D * 2;        // bytes per tile
-  __shared__ __attribute__((aligned(16))) char s_kv[3][4 * TB];   // stage: K0 K1 V0 V1
+  constexpr int SB = 4 * TB;               // bytes per stage: K0 K1 V0 V1
+  __shared__ __attribute__((aligned(16))) char s_kv[kPfStages * SB];
   __shared__ int s_pos[kPfEntries];        // first token position of each entry's page, -1 unusable
   __shared__ int s_phys[kPfEntries];
 
@@ -74,6 +93,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
+  const bool lag = w >= kPfWaves / 2;      // wave-uniform: the half-step-behind group
   const int j = lane & 31;                 // row within the wave
   const int hf = lane >> 5;                // lane half
   const int R = R0 + w * 32 + j;
@@ -96,7 +116,6 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
     }
   }
 
-  const int U = a.units;
   const int64_t cap = a.sel_capacity;
   const int e0 = (int)clampv<int64_t>(a.sel_indptr[u], 0, cap);
   const int e1 = (int)clampv<int64_t>(a.sel_indptr[u + 1], 0, cap);
@@ -105,9 +124,14 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
   const int tpp_log2 = a.tpp_log2;
   const int tpp = 1 << tpp_log2;
   const float c = a.scale_log2;
-  (void)U;
+  const float grow_thr = 8.f / c;          // max growth (raw score units) that forces a rescale
 
-  float m = -INFINITY;                     // running max of raw scores of row j
+  // The reference max m moves only when a row's max exceeds it by more than
+  // 2^8 in probability; numerator and sum share the reference, so the result
+  // is unchanged, and probabilities stay <= 256, far inside bf16/fp32. The
+  // start value is finite and below any score: the first visible key moves it.
+  float m = -1e30f;
+  float mc = m * c;
   float lsum = 0.f;
   f32x16 acc[NDB];
 #pragma unroll
@@ -130,7 +154,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
     const int nt = cn << tpp_log2;         // tiles in this chunk
     const int nsteps = (nt + 1) >> 1;
     // cooperative copy: thread t moves 16 B of K and 16 B of V of tile (t / 256)
-    const int ct = __builtin_amdgcn_readfirstlane(tid >> 8);   // tile of the step (per wave)
+    const int ct = tid >> 8;               // wave-uniform
     const int cb = (tid & 255) * 16;       // byte offset inside the tile (D = 128)
     auto tile_info = [&](int t, int& ph, int& pos) {
       if (t >= nt) { ph = -1; pos = -1; return; }
@@ -138,14 +162,33 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       ph = s_phys[e];
       pos = s_pos[e] < 0 ? -1 : s_pos[e] + (t & (tpp - 1)) * kTile;
     };
+    // step table of 64 steps from tb, one int per lane: (this wave's pool
+    // tile + 1) << 3 (0: unusable or past the chunk) | the step's flags (stop:
+    // every key of the step and later is past the block's last query; full:
+    // no masking needed; partial: this wave's tile ends past the context)
+    int tb = 0, tab = 0;
+    auto build_table = [&](int base) {
+      tb = base;
+      const int st = base + lane;
+      int ph0, pos0, ph1, pos1;
+      tile_info(2 * st, ph0, pos0);
+      tile_info(2 * st + 1, ph1, pos1);
+      const int mph = ct ? ph1 : ph0;
+      const int mpos = ct ? pos1 : pos0;
+      int f = mph >= 0 ? (mph * tpp + ((2 * st + ct) & (tpp - 1)) + 1) << 3 : 0;
+      if (pos0 > vis_hi || (pos0 < 0 && pos1 > vis_hi)) f |= kFlagStop;
+      if (ph0 >= 0 && ph1 >= 0 && pos1 + kTile - 1 <= vis_lo) f |= kFlagFull;
+      if (mph >= 0 && L - mpos < kTile) f |= kFlagPartial;
+      tab = f;
+    };
+    auto flags_of = [&](int st) { return __builtin_amdgcn_readlane(tab, st - tb); };
+    auto stage = [&](int x) -> char* { return s_kv + (x & (kPfStages - 1)) * SB; };
+
     // unusable tiles and bytes past the tile read as zeros (zero-range descriptor)
     auto load_step = [&](int st, s16x8& kx, s16x8& vx) {
-      int ph, pos;
-      tile_info(2 * st + ct, ph, pos);
-      ph = __builtin_amdgcn_readfirstlane(ph);        // wave-uniform: ct is per wave
-      const int64_t base =
-          uniform64(((int64_t)(ph < 0 ? 0 : ph) * P + (int64_t)((2 * st + ct) & (tpp - 1)) * kTile) * D);
-      const int range = ph >= 0 ? TB : 0;
+      const int tile = (int)((uint32_t)__builtin_amdgcn_readlane(tab, st - tb) >> 3) - 1;
+      const int64_t base = uniform64((int64_t)(tile < 0 ? 0 : tile) * (kTile * D));
+      const int range = tile >= 0 ? TB : 0;
       kx = __builtin_bit_cast(s16x8, __builtin_amdgcn_raw_buffer_load_b128(
                                          make_rsrc(a.k_pool + base, range), cb, 0, 0));
       vx = __builtin_bit_cast(s16x8, __builtin_amdgcn_raw_buffer_load_b128(
@@ -154,18 +197,19 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
     // V slots past the context are stored as zeros (their probability is 0,
     // and stale contents there must not reach the sum); 16 B = tokens
     // tok0 .. tok0 + 7 of one dimension
-    auto store_stage = [&](int st, int stage, const s16x8& kx, s16x8 vx) {
-      int ph, pos;
-      tile_info(2 * st + ct, ph, pos);
-      const int tok0 = (cb & 31) >> 1;
-      const int valid = L - pos;
-      if (ph >= 0 && valid < tok0 + 8) {
+    auto store_stage = [&](int st, const s16x8& kx, s16x8 vx) {
+      if (flags_of(st) & kFlagPartial) {
+        int ph, pos;
+        tile_info(2 * st + ct, ph, pos);
+        const int tok0 = (cb & 31) >> 1;
+        const int valid = L - pos;
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (tok0 + e >= valid) vx[e] = 0;
       }
       if (cb < TB) {
-        *reinterpret_cast<s16x8*>(&s_kv[stage][ct * TB + cb]) = kx;
+        char* sg = stage(st);
+        *reinterpret_cast<s16x8*>(sg + ct * TB + cb) = kx;
         // V row d (16 tokens) is stored in the operand's key order: half h
         // holds tokens 4h..4h+3 and 8+4h..8+4h+3, and sits at half
         // h ^ ((d >> 3) & 1) so that one 16-byte operand read of 32 rows hits
@@ -173,7 +217,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
         const int d = cb >> 5;
         const int q = (cb >> 4) & 1;
         const int sw = (d >> 3) & 1;
-        char* row = &s_kv[stage][2 * TB + ct * TB + d * 32];
+        char* row = sg + 2 * TB + ct * TB + d * 32;
         const s16x4 lo = {vx[0], vx[1], vx[2], vx[3]};   // tokens 8q + 0..3 -> half 0
         const s16x4 hi = {vx[4], vx[5], vx[6], vx[7]};   // tokens 8q + 4..7 -> half 1
         *reinterpret_cast<s16x4*>(row + ((0 ^ sw) * 16) + q * 8) = lo;
@@ -181,14 +225,8 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       }
     };
 
-    // Pipeline. LDS holds three key steps: the step being finished (its V),
-    // the next step (its K, for the next scores) and the step being copied in.
-    // Global loads run three steps ahead through three register sets. Within
-    // a step the exponentials of step st are interleaved with the score
-    // products of step st + 1, so the vector unit and the matrix cores work
-    // at the same time; then P.V of step st runs and the barrier closes it.
-    auto qk = [&](int stage) -> f32x16 {
-      const char* kb = s_kv[stage];
+    auto qk = [&](int x) -> f32x16 {
+      const char* kb = stage(x);
       f32x16 sacc = {};
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
@@ -198,31 +236,17 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       }
       return sacc;
     };
-    s16x8 kx0, vx0, kx1, vx1, kx2, vx2;
-    load_step(0, kx0, vx0);
-    load_step(1, kx1, vx1);
-    load_step(2, kx2, vx2);
-    store_stage(0, 0, kx0, vx0);
-    store_stage(1, 1, kx1, vx1);
-    __syncthreads();
-    f32x16 sa = qk(0), sb = {};
-
-    // one step; sc = stage of st, sn = stage of st + 1, sw = stage for st + 2;
-    // cur holds the scores of st, nxt receives those of st + 1.
-    // Returns false once every later key is past the block's last query.
-    auto body = [&](int st, int sc, int sn, int sw, s16x8& kl, s16x8& vl, const s16x8& ks,
-                    const s16x8& vs, f32x16& cur, f32x16& nxt) -> bool {
-      int ph0, pos0, ph1, pos1;
-      tile_info(2 * st, ph0, pos0);
-      tile_info(2 * st + 1, ph1, pos1);
-      if (pos0 > vis_hi || (pos0 < 0 && pos1 > vis_hi)) return false;   // block-uniform
+    // start of step st: stop test, loads of step st + 3, masking, row max and
+    // the (rare) rescale of everything accumulated so far
+    auto pre = [&](int st, f32x16& sv, s16x8& kl, s16x8& vl) -> bool {
+      const int fl = flags_of(st);
+      if (fl & kFlagStop) return false;    // block-uniform
       load_step(st + 3, kl, vl);           // this set's data (step st) is already in LDS
-      f32x16& sv = cur;
-
-      // lane's keys: kk(rr) = 8 * (rr / 4) + 4 * hf + rr % 4 (tile kk / 16);
-      // masked in place (no copy on the common, fully visible path)
-      const bool full = ph0 >= 0 && ph1 >= 0 && pos1 + kTile - 1 <= vis_lo;
-      if (!full) {
+      // lane's keys: kk(rr) = 8 * (rr / 4) + 4 * hf + rr % 4 (tile kk / 16)
+      if (!(fl & kFlagFull)) {
+        int ph0, pos0, ph1, pos1;
+        tile_info(2 * st, ph0, pos0);
+        tile_info(2 * st + 1, ph1, pos1);
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
           const int kk = 8 * (rr >> 2) + 4 * hf + (rr & 3);
@@ -230,58 +254,56 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
           if (!(tp >= 0 && tp + (kk & 15) <= vis_row)) sv[rr] = -INFINITY;
         }
       }
-      float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+      float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
 #pragma unroll
-      for (int rr = 4; rr < 16; rr += 2) mx = fmaxf(mx, fmaxf(sv[rr], sv[rr + 1]));
-      mx = fmaxf(mx, swap_halves(mx));
-      // The reference max m moves only when a row's max exceeds it by more
-      // than 2^8 in probability (the result is unchanged: numerator and sum
-      // share the reference; probabilities stay <= 256, far inside bf16/fp32).
-      const float m_new = fmaxf(m, mx);
-      const bool grow = m == -INFINITY ? m_new > m : (m_new - m) * c > 8.f;
-      if (__ballot(grow) != 0ull) {
-        const float mt = grow ? m_new : m;
-        const float alpha = (m == -INFINITY) ? 0.f : fast_exp2((m - mt) * c);
+      for (int rr = 3; rr < 15; rr += 2) mx = fmaxf(fmaxf(mx, sv[rr]), sv[rr + 1]);
+      mx = fmaxf(mx, sv[15]);
+      const float m_new = fmaxf(m, max_halves(mx));
+      if (__ballot(m_new - m > grow_thr) != 0ull) {
+        const float mt = m_new - m > grow_thr ? m_new : m;
+        const float alpha = fast_exp2((m - mt) * c);
         lsum *= alpha;
 #pragma unroll
         for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
         m = mt;
+        mc = m * c;
       }
-      const float mc = (m == -INFINITY) ? 0.f : m * c;
-
-      // exponentials of step st, interleaved with the scores of step st + 1
+      return true;
+    };
+    // exponentials of step st (into pb), interleaved with the scores of step st + 1
+    auto qk_exp = [&](int st, const f32x16& sv, f32x16& nxt, s16x8 (&pb)[2]) {
       float pv[16];
-      {
-        const char* kb = s_kv[sn];
-        f32x16 sn_acc = {};
+      const char* kb = stage(st + 1);
+      f32x16 sn_acc = {};
 #pragma unroll
-        for (int s2 = 0; s2 < KS; ++s2) {
-          const s16x8 kop = *reinterpret_cast<const s16x8*>(
-              kb + (j >> 4) * TB + (((2 * s2 + hf) * kTile + (j & 15)) * 16));
-          sn_acc = mfma32x32x16(kop, qreg[s2], sn_acc);
+      for (int s2 = 0; s2 < KS; ++s2) {
+        const s16x8 kop = *reinterpret_cast<const s16x8*>(
+            kb + (j >> 4) * TB + (((2 * s2 + hf) * kTile + (j & 15)) * 16));
+        sn_acc = mfma32x32x16(kop, qreg[s2], sn_acc);
 #pragma unroll
-          for (int e = 0; e < 16 / KS; ++e) {
-            const int rr = s2 * (16 / KS) + e;
-            pv[rr] = fast_exp2(fmaf(sv[rr], c, -mc));
-          }
+        for (int e = 0; e < 16 / KS; ++e) {
+          const int rr = s2 * (16 / KS) + e;
+          pv[rr] = fast_exp2(fmaf(sv[rr], c, -mc));
         }
-        nxt = sn_acc;
       }
+      nxt = sn_acc;
       {
         float t8[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) t8[i] = pv[i] + pv[i + 8];
         lsum += ((t8[0] + t8[4]) + (t8[1] + t8[5])) + ((t8[2] + t8[6]) + (t8[3] + t8[7]));
       }
-      s16x8 pb[2];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const s16x4 lo = pack_bf16x4(pv[8 * t], pv[8 * t + 1], pv[8 * t + 2], pv[8 * t + 3]);
         const s16x4 hi = pack_bf16x4(pv[8 * t + 4], pv[8 * t + 5], pv[8 * t + 6], pv[8 * t + 7]);
         pb[t] = (s16x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       }
-      // O^T += V^T . P^T; k-slot 8 hf + e of step t <-> key 16 t + (e < 4 ? 4 hf + e : 8 + 4 hf + e - 4)
-      const char* vb = s_kv[sc] + 2 * TB;
+    };
+    // O^T += V^T . P^T for step x; k-slot 8 hf + e of tile t <-> key
+    // 16 t + (e < 4 ? 4 hf + e : 8 + 4 hf + e - 4)
+    auto pv_step = [&](int x, const s16x8 (&pb)[2]) {
+      const char* vb = stage(x) + 2 * TB;
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
 #pragma unroll
@@ -292,24 +314,57 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
           acc[d] = mfma32x32x16(vop, pb[t], acc[d]);
         }
       }
-      if (st + 2 < nsteps) store_stage(st + 2, sw, ks, vs);
+    };
+
+    s16x8 kx0, vx0, kx1, vx1, kx2, vx2;
+    build_table(0);
+    load_step(0, kx0, vx0);
+    load_step(1, kx1, vx1);
+    load_step(2, kx2, vx2);
+    store_stage(0, kx0, vx0);
+    store_stage(1, kx1, vx1);
+    __syncthreads();
+    f32x16 sa = qk(0), sb = {};
+    s16x8 pb[2];                           // probabilities of the step waiting for P.V
+
+    // one step; kl: register set of step st (reloaded with st + 3), ks: set of
+    // st + 2 (stored now); cur holds the scores of st, nxt receives those of
+    // st + 1. Returns false once every later key is past the block's last query.
+    auto body = [&](int st, s16x8& kl, s16x8& vl, const s16x8& ks, const s16x8& vs,
+                    f32x16& cur, f32x16& nxt) -> bool {
+      if (st > 0 && (st & 31) == 0) build_table(st);
+      if (!lag) {
+        if (!pre(st, cur, kl, vl)) return false;
+        qk_exp(st, cur, nxt, pb);
+        pv_step(st, pb);
+        if (st + 2 < nsteps) store_stage(st + 2, ks, vs);
+      } else {
+        if (st > 0) pv_step(st - 1, pb);
+        if (st + 2 < nsteps) store_stage(st + 2, ks, vs);
+        if (!pre(st, cur, kl, vl)) return false;
+        qk_exp(st, cur, nxt, pb);
+      }
       __syncthreads();
       return true;
     };
-    // set and stage of step x: x % 3; score buffer of step x: x % 2
-    for (int st = 0; st < nsteps; st += 6) {
-      if (!body(st, 0, 1, 2, kx0, vx0, kx2, vx2, sa, sb)) { done = true; break; }
-      if (st + 1 >= nsteps) break;
-      if (!body(st + 1, 1, 2, 0, kx1, vx1, kx0, vx0, sb, sa)) { done = true; break; }
-      if (st + 2 >= nsteps) break;
-      if (!body(st + 2, 2, 0, 1, kx2, vx2, kx1, vx1, sa, sb)) { done = true; break; }
-      if (st + 3 >= nsteps) break;
-      if (!body(st + 3, 0, 1, 2, kx0, vx0, kx2, vx2, sb, sa)) { done = true; break; }
-      if (st + 4 >= nsteps) break;
-      if (!body(st + 4, 1, 2, 0, kx1, vx1, kx0, vx0, sa, sb)) { done = true; break; }
-      if (st + 5 >= nsteps) break;
-      if (!body(st + 5, 2, 0, 1, kx2, vx2, kx1, vx1, sb, sa)) { done = true; break; }
+    // register set of step x: x % 3; score buffer of step x: x % 2
+    int st = 0;
+    for (; st < nsteps; st += 6) {
+      if (!body(st, kx0, vx0, kx2, vx2, sa, sb)) { done = true; break; }
+      if (st + 1 >= nsteps) { st += 1; break; }
+      if (!body(st + 1, kx1, vx1, kx0, vx0, sb, sa)) { done = true; break; }
+      if (st + 2 >= nsteps) { st += 2; break; }
+      if (!body(st + 2, kx2, vx2, kx1, vx1, sa, sb)) { done = true; break; }
+      if (st + 3 >= nsteps) { st += 3; break; }
+      if (!body(st + 3, kx0, vx0, kx2, vx2, sb, sa)) { done = true; break; }
+      if (st + 4 >= nsteps) { st += 4; break; }
+      if (!body(st + 4, kx1, vx1, kx0, vx0, sa, sb)) { done = true; break; }
+      if (st + 5 >= nsteps) { st += 5; break; }
+      if (!body(st + 5, kx2, vx2, kx1, vx1, sb, sa)) { done = true; break; }
     }
+    // the lagging group still owes P.V of the chunk's last step (a stop
+    // happens before a step's exponentials, so nothing is owed then)
+    if (lag && !done) pv_step(nsteps - 1, pb);
   }
 
   const float ltot = lsum + swap_halves(lsum);

@@ -61,6 +61,7 @@ def _select(dims, params, cap=1 << 20, ws=None, ctx=FAKE, indptr=FAKE, pages=FAK
     (dict(head_dim=96), -2), (dict(page_size=24), -2), (dict(page_size=8), -2),
     (dict(num_q_heads=6, num_kv_heads=4), -1), (dict(num_requests=0), -1),
     (dict(max_q_len=0), -1), (dict(num_phys_pages=0), -1), (dict(num_requests=2000, num_kv_heads=8), -2),
+    (dict(num_phys_pages=1 << 28), -2), (dict(num_phys_pages=1 << 24, page_size=256), -2),
 ])
 def test_bad_dims_rejected(kw, code):
     params = B.spa_select_params_t(0, 4, 256, 0, 0, 0, 0, None, None)
