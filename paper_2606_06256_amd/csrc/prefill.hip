@@ -13,15 +13,18 @@
 // wave copies the next 64 steps' tile indices and flags into one register
 // (lane i <-> step i), read back with v_readlane, so no LDS round trip sits
 // in front of a step's loads. Keys stream in steps of 32 (two 16-token
-// tiles): each thread loads its share of a step's K and V tiles three steps
-// ahead into registers and stores it into one of four LDS stages. Per wave and
-// step:
+// tiles) through eight LDS stages: the K and V tiles of a step are copied from
+// HBM straight into LDS (buffer loads with the LDS destination) six steps
+// ahead, so no register staging and no LDS store instructions are needed.
+// Per wave and step:
 //   S^T[32 keys x 32 rows]  = K_step[32 x D] . Q^T       (D/16 steps, 32x32x16)
 //   O^T[D x 32 rows]       += V_step^T[D x 32] . P^T     (2 x D/32, 32x32x16)
 // In the S^T layout each lane holds 16 keys of one row, so the row max needs
 // one cross-half swap and the running max, the sum and the rescale are
-// lane-local; the 16 probabilities are, in order, the operand of the second
-// product (the key order inside a step is permuted identically for V).
+// lane-local. The probabilities of tokens 8h..8h+7 of a tile must sit in lane
+// half h to meet V rows in token order; the S^T layout leaves half h with
+// tokens 4h..4h+3 and 8+4h..8+4h+3, so one v_permlane32_swap per register pair
+// exchanges the middle two quarters.
 //
 // Waves w and w + 4 share a SIMD. Waves 4..7 run half a step behind: in the
 // interval between two barriers they first finish the previous step (its
@@ -52,11 +55,43 @@ __device__ __forceinline__ float swap_halves(float x) {
   return __uint_as_float(__lane_id() < 32 ? r[1] : r[0]);
 }
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// HBM -> LDS copy of 16 bytes per lane: bytes [voff, voff + 16) of the buffer
+// at `base` (range `bytes`; zero-range reads nothing) land at LDS byte
+// lds + 16 * lane. Inline assembly, so that the compiler does not wait for the
+// copy before each LDS read (it cannot tell the stages apart); the pipeline's
+// own waits order it. `base` and `lds` are wave-uniform.
+__device__ __forceinline__ void copy_to_lds(const void* base, int bytes, const void* lds, int voff) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  const v4i rs = {(int)__builtin_amdgcn_readfirstlane((uint32_t)b),
+                  (int)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu),
+                  __builtin_amdgcn_readfirstlane(bytes), 0x00020000};
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(m0v), "v"(voff), "s"(rs) : "m0");
+}
+
+// Barrier of the key-step pipeline: this wave's LDS accesses are complete and
+// so are its copies into LDS up to two steps ahead, while the copies of later
+// steps (two per step, N in all) stay in flight. (__syncthreads would wait for
+// every outstanding copy.)
+template <int N>
+__device__ __forceinline__ void step_barrier() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0070 | N);  // vmcnt(N) expcnt(7) lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 constexpr int kPfWaves = 8;
 constexpr int kPfThreads = kPfWaves * 64;
 constexpr int kPfRows = kPfWaves * 32;     // query rows per block
 constexpr int kPfEntries = 1024;           // translated page entries held in LDS
-constexpr int kPfStages = 4;               // LDS key steps
+constexpr int kPfStages = 8;               // LDS key steps
+constexpr int kPfAhead = 6;                // steps between a copy's issue and its use
 constexpr int kFlagStop = 1, kFlagFull = 2, kFlagPartial = 4;
 
 template <int D>
@@ -137,6 +172,11 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
 #pragma unroll
   for (int d = 0; d < NDB; ++d) acc[d] = (f32x16){};
 
+  // LDS starts as zeros: a copy of an unusable tile (zero-range descriptor)
+  // then leaves finite values behind, whatever the previous kernel left there
+  for (int i = tid * 16; i < (int)sizeof(s_kv); i += kPfThreads * 16)
+    *reinterpret_cast<s16x8*>(s_kv + i) = (s16x8){0, 0, 0, 0, 0, 0, 0, 0};
+
   bool done = false;
   for (int ce = 0; ce < n_e && !done; ce += kPfEntries) {
     const int cn = min(kPfEntries, n_e - ce);
@@ -153,9 +193,21 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
 
     const int nt = cn << tpp_log2;         // tiles in this chunk
     const int nsteps = (nt + 1) >> 1;
-    // cooperative copy: thread t moves 16 B of K and 16 B of V of tile (t / 256)
-    const int ct = tid >> 8;               // wave-uniform
-    const int cb = (tid & 255) * 16;       // byte offset inside the tile (D = 128)
+    // Copies: wave w moves 1 KiB of K and 1 KiB of V of tile ct = w / 4 of a
+    // step (D = 64: waves with part >= 2 have nothing to move). K keeps its
+    // pool layout. V row d (16 tokens, two 16-byte halves) keeps token order,
+    // with half h stored at h ^ ((d >> 3) & 1) so that one operand read of 32
+    // rows hits distinct LDS banks; lane l fills LDS slot part * 64 + l and so
+    // reads the pool half that belongs there.
+    const int ct = w >> 2;                 // wave-uniform
+    const int part = w & 3;
+    const bool mover = part * 1024 < TB;   // wave-uniform
+    const int k_off = part * 1024 + lane * 16;
+    const int v_off = [&] {
+      const int slot = part * 64 + lane;
+      const int d = slot >> 1;
+      return d * 32 + (((slot & 1) ^ ((d >> 3) & 1)) * 16);
+    }();
     auto tile_info = [&](int t, int& ph, int& pos) {
       if (t >= nt) { ph = -1; pos = -1; return; }
       const int e = t >> tpp_log2;
@@ -167,9 +219,14 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
     // every key of the step and later is past the block's last query; full:
     // no masking needed; partial: this wave's tile ends past the context)
     int tb = 0, tab = 0;
+    // (rare paths take the lane index through an empty asm, so that the
+    // compiler does not hoist their address arithmetic into registers that
+    // stay live across the whole loop)
+    auto opaque = [](int x) { asm volatile("" : "+v"(x)); return x; };
     auto build_table = [&](int base) {
       tb = base;
-      const int st = base + lane;
+      const int ln = opaque(lane);
+      const int st = base + ln;
       int ph0, pos0, ph1, pos1;
       tile_info(2 * st, ph0, pos0);
       tile_info(2 * st + 1, ph1, pos1);
@@ -184,45 +241,34 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
     auto flags_of = [&](int st) { return __builtin_amdgcn_readlane(tab, st - tb); };
     auto stage = [&](int x) -> char* { return s_kv + (x & (kPfStages - 1)) * SB; };
 
-    // unusable tiles and bytes past the tile read as zeros (zero-range descriptor)
-    auto load_step = [&](int st, s16x8& kx, s16x8& vx) {
-      const int tile = (int)((uint32_t)__builtin_amdgcn_readlane(tab, st - tb) >> 3) - 1;
+    // HBM -> LDS copy of this wave's share of step x; unusable tiles use a
+    // zero-range descriptor (no bytes are read)
+    auto issue_copy = [&](int x) {
+      if (!mover) return;
+      const int tile = (int)((uint32_t)__builtin_amdgcn_readlane(tab, x - tb) >> 3) - 1;
       const int64_t base = uniform64((int64_t)(tile < 0 ? 0 : tile) * (kTile * D));
       const int range = tile >= 0 ? TB : 0;
-      kx = __builtin_bit_cast(s16x8, __builtin_amdgcn_raw_buffer_load_b128(
-                                         make_rsrc(a.k_pool + base, range), cb, 0, 0));
-      vx = __builtin_bit_cast(s16x8, __builtin_amdgcn_raw_buffer_load_b128(
-                                         make_rsrc(a.v_pool + base, range), cb, 0, 0));
+      const char* sg = stage(x);
+      copy_to_lds(a.k_pool + base, range, sg + ct * TB + part * 1024, k_off);
+      copy_to_lds(a.v_pool + base, range, sg + 2 * TB + ct * TB + part * 1024, v_off);
     };
-    // V slots past the context are stored as zeros (their probability is 0,
-    // and stale contents there must not reach the sum); 16 B = tokens
-    // tok0 .. tok0 + 7 of one dimension
-    auto store_stage = [&](int st, const s16x8& kx, s16x8 vx) {
-      if (flags_of(st) & kFlagPartial) {
-        int ph, pos;
-        tile_info(2 * st + ct, ph, pos);
-        const int tok0 = (cb & 31) >> 1;
-        const int valid = L - pos;
+    // A tile that ends past the context: its V slots there are rewritten as
+    // zeros (their probability is 0, and stale contents there must not reach
+    // the sum). Runs before the barrier that publishes step x; waiting for
+    // this wave's loads also orders it after the copy into the same slots.
+    auto fix_partial = [&](int x) {
+      if (!mover || !(flags_of(x) & kFlagPartial)) return;
+      int ph, pos;
+      tile_info(2 * x + ct, ph, pos);
+      const int64_t base = uniform64((int64_t)(ph * tpp + ((2 * x + ct) & (tpp - 1))) * (kTile * D));
+      s16x8 vx = __builtin_bit_cast(s16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                                               make_rsrc(a.v_pool + base, TB), v_off, 0, 0));
+      const int tok0 = (v_off & 16) >> 1;  // this lane's 8 tokens start here
+      const int valid = L - pos;
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (tok0 + e >= valid) vx[e] = 0;
-      }
-      if (cb < TB) {
-        char* sg = stage(st);
-        *reinterpret_cast<s16x8*>(sg + ct * TB + cb) = kx;
-        // V row d (16 tokens) is stored in the operand's key order: half h
-        // holds tokens 4h..4h+3 and 8+4h..8+4h+3, and sits at half
-        // h ^ ((d >> 3) & 1) so that one 16-byte operand read of 32 rows hits
-        // distinct LDS banks. This thread holds tokens 8q..8q+7 of row d.
-        const int d = cb >> 5;
-        const int q = (cb >> 4) & 1;
-        const int sw = (d >> 3) & 1;
-        char* row = sg + 2 * TB + ct * TB + d * 32;
-        const s16x4 lo = {vx[0], vx[1], vx[2], vx[3]};   // tokens 8q + 0..3 -> half 0
-        const s16x4 hi = {vx[4], vx[5], vx[6], vx[7]};   // tokens 8q + 4..7 -> half 1
-        *reinterpret_cast<s16x4*>(row + ((0 ^ sw) * 16) + q * 8) = lo;
-        *reinterpret_cast<s16x4*>(row + ((1 ^ sw) * 16) + q * 8) = hi;
-      }
+      for (int e = 0; e < 8; ++e)
+        if (tok0 + e >= valid) vx[e] = 0;
+      *reinterpret_cast<s16x8*>(stage(x) + 2 * TB + ct * TB + part * 1024 + lane * 16) = vx;
     };
 
     auto qk = [&](int x) -> f32x16 {
@@ -236,12 +282,12 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       }
       return sacc;
     };
-    // start of step st: stop test, loads of step st + 3, masking, row max and
-    // the (rare) rescale of everything accumulated so far
-    auto pre = [&](int st, f32x16& sv, s16x8& kl, s16x8& vl) -> bool {
+    // start of step st: stop test, copy of step st + kPfAhead, masking, row
+    // max and the (rare) rescale of everything accumulated so far
+    auto pre = [&](int st, f32x16& sv) -> bool {
       const int fl = flags_of(st);
       if (fl & kFlagStop) return false;    // block-uniform
-      load_step(st + 3, kl, vl);           // this set's data (step st) is already in LDS
+      issue_copy(st + kPfAhead);
       // lane's keys: kk(rr) = 8 * (rr / 4) + 4 * hf + rr % 4 (tile kk / 16)
       if (!(fl & kFlagFull)) {
         int ph0, pos0, ph1, pos1;
@@ -293,15 +339,21 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
         for (int i = 0; i < 8; ++i) t8[i] = pv[i] + pv[i + 8];
         lsum += ((t8[0] + t8[4]) + (t8[1] + t8[5])) + ((t8[2] + t8[6]) + (t8[3] + t8[7]));
       }
+      // tile t: lo = tokens 4 hf + 0..3, hi = tokens 8 + 4 hf + 0..3; after the
+      // swap half 0 holds tokens 0..7 and half 1 tokens 8..15
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const s16x4 lo = pack_bf16x4(pv[8 * t], pv[8 * t + 1], pv[8 * t + 2], pv[8 * t + 3]);
         const s16x4 hi = pack_bf16x4(pv[8 * t + 4], pv[8 * t + 5], pv[8 * t + 6], pv[8 * t + 7]);
-        pb[t] = (s16x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const auto l2 = __builtin_bit_cast(uint32_t __attribute__((ext_vector_type(2))), lo);
+        const auto h2 = __builtin_bit_cast(uint32_t __attribute__((ext_vector_type(2))), hi);
+        const auto x0 = __builtin_amdgcn_permlane32_swap(l2[0], h2[0], false, false);
+        const auto x1 = __builtin_amdgcn_permlane32_swap(l2[1], h2[1], false, false);
+        const uint32_t __attribute__((ext_vector_type(4))) op = {x0[0], x1[0], x0[1], x1[1]};
+        pb[t] = __builtin_bit_cast(s16x8, op);
       }
     };
-    // O^T += V^T . P^T for step x; k-slot 8 hf + e of tile t <-> key
-    // 16 t + (e < 4 ? 4 hf + e : 8 + 4 hf + e - 4)
+    // O^T += V^T . P^T for step x: k-slot 8 hf + e of tile t is token 8 hf + e
     auto pv_step = [&](int x, const s16x8 (&pb)[2]) {
       const char* vb = stage(x) + 2 * TB;
 #pragma unroll
@@ -316,56 +368,46 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       }
     };
 
-    s16x8 kx0, vx0, kx1, vx1, kx2, vx2;
     build_table(0);
-    load_step(0, kx0, vx0);
-    load_step(1, kx1, vx1);
-    load_step(2, kx2, vx2);
-    store_stage(0, kx0, vx0);
-    store_stage(1, kx1, vx1);
-    __syncthreads();
+#pragma unroll
+    for (int x = 0; x < kPfAhead; ++x) issue_copy(x);
+    fix_partial(0);
+    fix_partial(1);
+    step_barrier<2 * (kPfAhead - 2)>();    // steps 0 and 1 are in LDS
     f32x16 sa = qk(0), sb = {};
     s16x8 pb[2];                           // probabilities of the step waiting for P.V
 
-    // one step; kl: register set of step st (reloaded with st + 3), ks: set of
-    // st + 2 (stored now); cur holds the scores of st, nxt receives those of
-    // st + 1. Returns false once every later key is past the block's last query.
-    auto body = [&](int st, s16x8& kl, s16x8& vl, const s16x8& ks, const s16x8& vs,
-                    f32x16& cur, f32x16& nxt) -> bool {
+    // one step; cur holds the scores of st, nxt receives those of st + 1.
+    // Returns false once every later key is past the block's last query.
+    auto body = [&](int st, f32x16& cur, f32x16& nxt) -> bool {
       if (st > 0 && (st & 31) == 0) build_table(st);
       if (!lag) {
-        if (!pre(st, cur, kl, vl)) return false;
+        if (!pre(st, cur)) return false;
         qk_exp(st, cur, nxt, pb);
         pv_step(st, pb);
-        if (st + 2 < nsteps) store_stage(st + 2, ks, vs);
+        fix_partial(st + 2);
       } else {
         if (st > 0) pv_step(st - 1, pb);
-        if (st + 2 < nsteps) store_stage(st + 2, ks, vs);
-        if (!pre(st, cur, kl, vl)) return false;
+        fix_partial(st + 2);
+        if (!pre(st, cur)) return false;
         qk_exp(st, cur, nxt, pb);
       }
-      __syncthreads();
+      step_barrier<2 * (kPfAhead - 2)>();
       return true;
     };
-    // register set of step x: x % 3; score buffer of step x: x % 2
-    int st = 0;
-    for (; st < nsteps; st += 6) {
-      if (!body(st, kx0, vx0, kx2, vx2, sa, sb)) { done = true; break; }
-      if (st + 1 >= nsteps) { st += 1; break; }
-      if (!body(st + 1, kx1, vx1, kx0, vx0, sb, sa)) { done = true; break; }
-      if (st + 2 >= nsteps) { st += 2; break; }
-      if (!body(st + 2, kx2, vx2, kx1, vx1, sa, sb)) { done = true; break; }
-      if (st + 3 >= nsteps) { st += 3; break; }
-      if (!body(st + 3, kx0, vx0, kx2, vx2, sb, sa)) { done = true; break; }
-      if (st + 4 >= nsteps) { st += 4; break; }
-      if (!body(st + 4, kx1, vx1, kx0, vx0, sa, sb)) { done = true; break; }
-      if (st + 5 >= nsteps) { st += 5; break; }
-      if (!body(st + 5, kx2, vx2, kx1, vx1, sb, sa)) { done = true; break; }
+    // score buffer of step x: x % 2
+    bool stopped = false;
+    for (int st = 0; st < nsteps; st += 2) {
+      if (!body(st, sa, sb)) { stopped = true; break; }
+      if (st + 1 >= nsteps) break;
+      if (!body(st + 1, sb, sa)) { stopped = true; break; }
     }
     // the lagging group still owes P.V of the chunk's last step (a stop
     // happens before a step's exponentials, so nothing is owed then)
-    if (lag && !done) pv_step(nsteps - 1, pb);
+    if (lag && !stopped) pv_step(nsteps - 1, pb);
+    done = stopped;
   }
+  __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0): no copy into LDS outlives the block
 
   const float ltot = lsum + swap_halves(lsum);
   if (!row_ok) return;
