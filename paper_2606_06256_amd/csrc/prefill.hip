@@ -319,6 +319,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
     // exponentials of step st (into pb), interleaved with the scores of step st + 1
     auto qk_exp = [&](int st, const f32x16& sv, f32x16& nxt, s16x8 (&pb)[2]) {
       float pv[16];
+      __builtin_amdgcn_s_setprio(1);
       const char* kb = stage(st + 1);
       f32x16 sn_acc = {};
 #pragma unroll
@@ -333,6 +334,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
         }
       }
       nxt = sn_acc;
+      __builtin_amdgcn_s_setprio(0);
       {
         float t8[8];
 #pragma unroll
@@ -354,7 +356,10 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       }
     };
     // O^T += V^T . P^T for step x: k-slot 8 hf + e of tile t is token 8 hf + e
+    // (the matrix-core sections of a wave run at raised issue priority, so
+    // that the SIMD's other wave fills their gaps rather than delaying them)
     auto pv_step = [&](int x, const s16x8 (&pb)[2]) {
+      __builtin_amdgcn_s_setprio(1);
       const char* vb = stage(x) + 2 * TB;
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -366,6 +371,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
           acc[d] = mfma32x32x16(vop, pb[t], acc[d]);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
     };
 
     build_table(0);
