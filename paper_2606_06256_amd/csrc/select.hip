@@ -306,7 +306,10 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
 // (q_bar . ksum[phys(p)]) / n_valid(p) in float64, q_bar = sum over the G query
 // heads of the request's last query token. Eight lanes per page.
 __global__ __launch_bounds__(256) void select_score_kernel(const SelArgs a) {
+  constexpr int BS = 256;
+  constexpr int kRows = 8;            // pages per lane group loaded before any arithmetic
   __shared__ double s_qbar[128];
+  __shared__ int s_ph[BS];
   const int u = blockIdx.y;
   const int r = u / a.Hkv;
   const int g = u - r * a.Hkv;
@@ -315,7 +318,7 @@ __global__ __launch_bounds__(256) void select_score_kernel(const SelArgs a) {
   const int max_tokens = a.max_segs * a.pps * P;
   const int L = clampv(a.ctx_lens[r], 0, max_tokens);
   const int n = (L + P - 1) / P;
-  const int p_block = blockIdx.x * 256;
+  const int p_block = blockIdx.x * BS;
   if (p_block >= n) return;
   const int q0 = clampv(a.q_indptr[r], 0, a.total_q);
   const int q1 = clampv(a.q_indptr[r + 1], q0, a.total_q);
@@ -328,36 +331,62 @@ __global__ __launch_bounds__(256) void select_score_kernel(const SelArgs a) {
     }
     s_qbar[tid] = s;
   }
+  // every page of the block translated at once (one per thread), so the
+  // key-sum loads below do not wait on a table lookup each
+  {
+    const int p = p_block + tid;
+    const int32_t* seg_row = a.seg_table + (int64_t)u * a.max_segs;
+    s_ph[tid] = p < n ? translate_page(seg_row, a.page_table, p, a.pps, a.max_segs, a.n_virtual, a.n_phys)
+                      : -1;
+  }
   __syncthreads();
+  // 16 lanes per page, D / 16 consecutive floats each (two or one 16-byte loads)
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int sub = lane & 7;           // lane within the page group
-  const int per = D / 8;              // floats per lane (16 or 8)
-  const int32_t* seg_row = a.seg_table + (int64_t)u * a.max_segs;
+  const int grp = lane >> 4;          // page within a row of 4
+  const int sub = lane & 15;
+  const int per = D / 16;
+  double qb[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) qb[i] = i < per ? s_qbar[sub * per + i] : 0.0;
   uint64_t* keys = a.score_keys + (int64_t)u * a.max_pages;
-  for (int it = 0; it < 8; ++it) {
-    const int p = p_block + it * 32 + wave * 8 + (lane >> 3);
-    const bool valid = p < n;
-    const int ph = valid ? translate_page(seg_row, a.page_table, p, a.pps, a.max_segs, a.n_virtual,
-                                          a.n_phys)
-                         : -1;
-    double dot = 0.0;
-    if (ph >= 0) {
-      const float* ks = a.page_ksum + (int64_t)ph * D + sub * per;
-      for (int i = 0; i < per; i += 4) {
-        const float4 v = *reinterpret_cast<const float4*>(ks + i);
-        dot = fma((double)v.x, s_qbar[sub * per + i], dot);
-        dot = fma((double)v.y, s_qbar[sub * per + i + 1], dot);
-        dot = fma((double)v.z, s_qbar[sub * per + i + 2], dot);
-        dot = fma((double)v.w, s_qbar[sub * per + i + 3], dot);
+  // wave w covers block pages [64 w, 64 w + 64): rows of 4 pages
+  for (int r0 = 0; r0 < 16; r0 += kRows) {
+    float4 v[kRows][2];
+#pragma unroll
+    for (int k = 0; k < kRows; ++k) {
+      const int ph = s_ph[wave * 64 + (r0 + k) * 4 + grp];
+      const float4 z = {0.f, 0.f, 0.f, 0.f};
+      v[k][0] = z;
+      v[k][1] = z;
+      if (ph >= 0) {
+        const float* ks = a.page_ksum + (int64_t)ph * D + sub * per;
+        v[k][0] = *reinterpret_cast<const float4*>(ks);
+        if (per == 8) v[k][1] = *reinterpret_cast<const float4*>(ks + 4);
       }
     }
-    dot += __shfl_xor(dot, 1);
-    dot += __shfl_xor(dot, 2);
-    dot += __shfl_xor(dot, 4);
-    if (valid && sub == 0) {
-      const int nvalid = min(P, L - p * P);
-      keys[p] = ph >= 0 ? descending_key(dot / (double)nvalid) : ~0ull;
+#pragma unroll
+    for (int k = 0; k < kRows; ++k) {
+      double dot = 0.0;
+      dot = fma((double)v[k][0].x, qb[0], dot);
+      dot = fma((double)v[k][0].y, qb[1], dot);
+      dot = fma((double)v[k][0].z, qb[2], dot);
+      dot = fma((double)v[k][0].w, qb[3], dot);
+      dot = fma((double)v[k][1].x, qb[4], dot);
+      dot = fma((double)v[k][1].y, qb[5], dot);
+      dot = fma((double)v[k][1].z, qb[6], dot);
+      dot = fma((double)v[k][1].w, qb[7], dot);
+      dot += __shfl_xor(dot, 1);
+      dot += __shfl_xor(dot, 2);
+      dot += __shfl_xor(dot, 4);
+      dot += __shfl_xor(dot, 8);
+      const int pi = wave * 64 + (r0 + k) * 4 + grp;
+      const int p = p_block + pi;
+      if (sub == 0 && p < n) {
+        const int ph = s_ph[pi];
+        const int nvalid = min(P, L - p * P);
+        keys[p] = ph >= 0 ? descending_key(dot / (double)nvalid) : ~0ull;
+      }
     }
   }
 }

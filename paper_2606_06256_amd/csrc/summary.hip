@@ -18,13 +18,22 @@ __global__ __launch_bounds__(256) void page_summary_kernel(const SummaryArgs a) 
   const int nv = clampv(a.page_valid[page], 0, P);
   double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   const __bf16* base = a.k_pool + page * (int64_t)P * D;
-  for (int t = 0; t < nv; ++t) {
-    const int tile = t >> 4;
-    const int uu = t & 15;
-    const s16x8 v = *reinterpret_cast<const s16x8*>(base + (int64_t)tile * kTile * D +
-                                                     (c * kTile + uu) * 8);
+  // a tile's 16 tokens are loaded before any is added (16 loads in flight);
+  // tokens past nv are read but not added. bf16 values of a page sum exactly
+  // in float64, so the order of the additions does not matter.
+  const int ntiles = (nv + kTile - 1) / kTile;
+  for (int tile = 0; tile < ntiles; ++tile) {
+    const __bf16* tp = base + (int64_t)tile * kTile * D + c * kTile * 8;
+    s16x8 v[kTile];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] += (double)bf16_bits_to_float((uint16_t)v[e]);
+    for (int uu = 0; uu < kTile; ++uu) v[uu] = *reinterpret_cast<const s16x8*>(tp + uu * 8);
+#pragma unroll
+    for (int uu = 0; uu < kTile; ++uu) {
+      if (tile * kTile + uu < nv) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += (double)bf16_bits_to_float((uint16_t)v[uu][e]);
+      }
+    }
   }
   float4 lo4 = make_float4((float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]);
   float4 hi4 = make_float4((float)acc[4], (float)acc[5], (float)acc[6], (float)acc[7]);
