@@ -371,6 +371,15 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
           acc[d] = mfma32x32x16(vop, pb[t], acc[d]);
         }
       }
+      // operand reads run four products ahead: 4 reads, then (product, read)
+      // pairs, then the last 4 products
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int i = 0; i < 2 * NDB - 4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x8, 4, 0);
       __builtin_amdgcn_s_setprio(0);
     };
 
