@@ -359,7 +359,8 @@ def build(spec: Spec) -> Workload:
 # the five named workloads
 # --------------------------------------------------------------------------
 def config_spec(i: int) -> Spec:
-    """Named workloads 1..5 (shapes of the paper's Llama/Qwen-style layers)."""
+    """Named workloads 1..9 (shapes of the paper's Llama/Qwen-style layers;
+    6..9 are the head-class micro-benchmark shape of Section 5.3)."""
     seed = 1000 + i
     if i == 1:
         return Spec(name="tiny", B=1, Hq=4, Hkv=4, D=64, P=16, seg_tokens=256,
@@ -401,7 +402,27 @@ def config_spec(i: int) -> Spec:
                     description="batch 32 decode, 64/8 heads, D128, 128K context, segment 8192, "
                     "page 32, top-10% pages by (sum of group queries) . mean key; 2% of pages "
                     "shifted by +3 along a seeded direction")
+    if i in (6, 7, 8):
+        return headclass_spec(i, {6: 8192, 7: 32768, 8: 131072}[i], q_len=1)
+    if i == 9:
+        return headclass_spec(i, 32768, q_len=512)
     raise ValueError(f"no workload {i}")
+
+
+def headclass_spec(i: int, ctx: int, q_len: int, layers: int = 64) -> Spec:
+    """The paper's own micro-benchmark shape: Qwen3-32B-like layers (32/8
+    heads, D128), half of the KV heads global (all pages) and half local
+    (4 sink tokens + a 316-token window: a 320-token window), run for 64
+    layers as one batched call (each layer is one request of the batch: its
+    own segment table rows and pages)."""
+    kind = "decode" if q_len == 1 else f"prefill of a {q_len}-token chunk"
+    return Spec(name=f"qwen3_32b_headclass_{'decode' if q_len == 1 else 'prefill'}_{ctx // 1024}k",
+                B=layers, Hq=32, Hkv=8, D=128, P=16, seg_tokens=2048,
+                ctx_lens=[ctx] * layers, q_lens=[q_len] * layers, seed=1000 + i,
+                sel_mode=SEL_HEAD_CLASS, head_policy=[1, 0] * 4, n_sink=4, window=316,
+                description=f"{layers} layers x 1 request (one batched call), 32/8 heads, D128, "
+                            f"{ctx // 1024}K context in 2048-token segments, page 16, {kind}; "
+                            f"KV heads alternate global (all pages) / local (sink 4 + window 316)")
 
 
 def config(i: int) -> Workload:

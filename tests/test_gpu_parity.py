@@ -44,6 +44,14 @@ def test_scaled_decode_configs(i, div, batch):
     PU.run_parity(I.build(I.scaled_spec(i, div, batch)), label=f"cfg{i}/div{div}")
 
 
+@pytest.mark.parametrize("i,div,batch", [(6, 1, 4), (7, 8, 3), (8, 32, 2), (9, 16, 3)])
+def test_scaled_headclass_configs(i, div, batch):
+    """The head-class micro-benchmark shape (global and local KV heads, one
+    batched call over layers), decode and chunked prefill, at reduced sizes."""
+    _require_gpu()
+    PU.run_parity(I.build(I.scaled_spec(i, div, batch)), label=f"cfg{i}/div{div}")
+
+
 def test_scaled_prefill_config():
     _require_gpu()
     sp = I.scaled_spec(4, 32, 2)
@@ -270,7 +278,7 @@ def test_validate_reports_bad_lists():
 # --------------------------------------------------------------------------
 # full-size workloads in the benchmark's launch configuration
 # --------------------------------------------------------------------------
-@pytest.mark.parametrize("i", [2, 3, 4, 5])
+@pytest.mark.parametrize("i", [2, 3, 4, 5, 6, 7, 8, 9])
 def test_full_size_config(i):
     _require_gpu()
     wl = I.config(i)
