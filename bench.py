@@ -11,7 +11,8 @@ Output: one JSON line. `value` is attended KV tokens per second for the whole
 step (inputs resident in HBM). `roofline` is the dominant kernel
 (decode_attn): algorithmic bytes per launch over its mean launch time,
 measured with HIP events on the launch stream. `cpu_baseline` is the fp64
-oracle timed on this host's cores on a sample of the same step.
+oracle timed on this host's cores (a pool of single-threaded processes) on
+a sample of the same step.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N] [--no-cpu-baseline]
 """
@@ -169,46 +170,62 @@ def attention_flops(wl, sel_indptr, sel_pages):
     return 4 * wl.D * tot
 
 
-def cpu_baseline(wl, min_seconds=10.0, max_seconds=30.0):
-    """fp64 oracle (select + attention) on a sample of the step's units."""
+def _cpu_worker(args):
+    """One process of the CPU baseline: the fp64 oracle (select + attention)
+    over its units, repeated until `seconds` have passed; single-threaded."""
+    cfg, units, seconds = args
     from threadpoolctl import threadpool_limits
 
     from oracle import segpa_oracle as O
-    sys.path.insert(0, os.path.join(ROOT, "tests"))
-    U = wl.num_units
-    n_sample = min(U, 32)
-    step = max(1, U // n_sample)
-    units = list(range(0, U, step))[:n_sample]
-    q64 = wl.q("cpu").double().numpy()
-    kv = {u: wl.unit_kv(*divmod(u, wl.Hkv), "cpu") for u in units}   # bf16, not timed
+    from paper_2606_06256_amd import inputs as I
+    wl = I.config(cfg)
     sp = wl.spec
-    tokens = 0
-    passes = 0
-    t0 = time.perf_counter()
     with threadpool_limits(limits=1):
-        while True:
+        q64 = wl.q("cpu").double().numpy()
+        kv = {}
+        for u in units:                     # input generation is not timed
+            K, V = wl.unit_kv(*divmod(u, wl.Hkv), "cpu")
+            kv[u] = (K.double().numpy(), V.double().numpy())
+        tokens = 0
+        done = 0
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < seconds:
             for u in units:
-                r, g = divmod(u, wl.Hkv)
-                K = kv[u][0].double().numpy()
-                V = kv[u][1].double().numpy()
+                K, V = kv[u]
                 sel = O.select(sp.sel_mode, wl.ctx_lens, wl.q_indptr, wl.Hq, wl.Hkv, wl.P,
                                budgets=wl.budgets, forced_head=sp.forced_head,
                                forced_tail=sp.forced_tail, seed=sp.sel_seed,
                                head_policy=wl.head_policy, n_sink=sp.n_sink, window=sp.window,
                                q=q64, kv_of_unit=lambda rr, gg: (K, V), units=[u])[u]
                 O.forward_unit(q64, wl.q_indptr, wl.ctx_lens, wl.Hq, wl.Hkv, wl.P, u, sel, K, V)
-                L = int(wl.ctx_lens[r])
+                L = int(wl.ctx_lens[u // wl.Hkv])
                 tokens += int(sum(min(wl.P, L - p * wl.P) for p in sel))
-                if time.perf_counter() - t0 > max_seconds:
-                    break
-            passes += 1
-            el = time.perf_counter() - t0
-            if el >= min_seconds or el > max_seconds:
-                break
-    el = time.perf_counter() - t0
-    return {"value": tokens / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{len(units)} of {U} (request, KV head) units of one step, {passes} pass(es), "
-                      f"{el:.1f} s, fp64 numpy single thread"}
+                done += 1
+        return tokens, time.perf_counter() - t0, done
+
+
+def cpu_baseline(cfg, wl, seconds=12.0, max_procs=16):
+    """fp64 oracle (select + attention) on a sample of the step's units, in a
+    pool of single-threaded processes over the host cores available to this
+    process (at most max_procs), all timed over the same interval."""
+    import multiprocessing as mp
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    procs = max(1, min(max_procs, cores))
+    U = wl.num_units
+    n_sample = min(U, 2 * procs)
+    units = sorted({int(x) for x in np.linspace(0, U - 1, n_sample)})
+    shares = [units[i::procs] for i in range(procs)]
+    shares = [sh for sh in shares if sh]
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(len(shares)) as pool:
+        res = pool.map(_cpu_worker, [(cfg, sh, seconds) for sh in shares])
+    tokens = sum(r[0] for r in res)
+    wall = max(r[1] for r in res)
+    done = sum(r[2] for r in res)
+    return {"value": tokens / wall, "unit": "tokens/s", "cores": len(shares), "kind": "oracle",
+            "sample": f"{len(units)} of {U} (request, KV head) units of one step, {done} unit "
+                      f"evaluations in {wall:.1f} s by {len(shares)} single-threaded fp64 numpy "
+                      f"processes (host cores available: {cores})"}
 
 
 def main():
@@ -254,7 +271,7 @@ def main():
     wl = I.config(args.workload)
 
     # CPU baseline first, before anything initialises the GPU
-    cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, wl)
 
     import torch
     from paper_2606_06256_amd import binding, build_lib

@@ -73,3 +73,11 @@ def test_code_text_ignores_comments_only():
     c = "int x = 1;\nint y = 3;"
     assert bench._code_text(a) == bench._code_text(b)
     assert bench._code_text(a) != bench._code_text(c)
+
+
+def test_cpu_baseline_pool_reports_what_it_used():
+    from paper_2606_06256_amd import inputs as I
+    r = bench.cpu_baseline(1, I.config(1), seconds=0.5, max_procs=2)
+    assert r["kind"] == "oracle" and r["unit"] == "tokens/s"
+    assert r["cores"] == 2 and r["value"] > 0
+    assert "2 single-threaded" in r["sample"]
