@@ -188,6 +188,26 @@ spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int
                                 size_t workspace_bytes, void* stream);
 
 /*
+ * RoPE positional alignment of cached keys (Section 4.2): a key cached at
+ * offline position p_off and reused at online position p_on is replaced by
+ * R(p_on) R(p_off)^-1 K(p_off), which is the rotation by delta = p_on - p_off.
+ * Each listed physical page of k_pool is rotated in place by its delta; every
+ * token slot of the page is rotated. Plane i pairs head dimension i with
+ * i + D/2 and turns by delta * rope_base^(-2 i / D). Arithmetic in float64,
+ * one rounding to bf16 (to nearest, ties to even).
+ * In:  pages device int32 [n]: distinct physical page ids (an id outside
+ *      [0, num_phys_pages) is skipped; an id listed twice is a data race);
+ *      deltas device int32 [n]; rope_base > 1 (10000 and 1e6 are common).
+ * In/out: k_pool device bf16 [num_phys_pages, P * D] in the tile layout.
+ * Errors: INVALID_ARG for a null pointer with n > 0, n < 0 or n >= 2^31, a
+ * rope_base that is not finite or <= 1, or a misaligned k_pool.
+ * Asynchronous on stream; n = 0 launches nothing.
+ */
+spa_status_t seg_paged_attn_rope_align(const spa_dims_t* dims, void* k_pool, const int32_t* pages,
+                                       const int32_t* deltas, int64_t n, double rope_base,
+                                       void* stream);
+
+/*
  * Page key summary for TOPK_MEANKEY (this build's content rule; the paper
  * states none): page_ksum[p][d] = float32 rounding of the sum over the first
  * page_valid_tokens[p] tokens of physical page p of K[token][d], accumulated in

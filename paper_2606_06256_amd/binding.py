@@ -66,6 +66,9 @@ def lib() -> ctypes.CDLL:
                                      ctypes.c_int64, _P, _P, _P, ctypes.c_size_t, _P]
     L.seg_paged_attn_page_summary.restype = ctypes.c_int
     L.seg_paged_attn_page_summary.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P]
+    L.seg_paged_attn_rope_align.restype = ctypes.c_int
+    L.seg_paged_attn_rope_align.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, ctypes.c_int64,
+                                             ctypes.c_double, _P]
     L.seg_paged_attn_validate.restype = ctypes.c_int
     L.seg_paged_attn_validate.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P, _P, _P,
                                           ctypes.c_int64, ctypes.POINTER(ctypes.c_int32),
@@ -162,6 +165,17 @@ def seg_paged_attn_page_summary(dims: spa_dims_t, k_pool, page_valid_tokens, pag
         _ptr(page_valid_tokens, torch.int32, "page_valid_tokens"),
         _ptr(page_ksum, torch.float32, "page_ksum"), _stream(stream))
     _check("seg_paged_attn_page_summary", st)
+
+
+def seg_paged_attn_rope_align(dims: spa_dims_t, k_pool, pages, deltas, rope_base: float = 10000.0,
+                              stream=None):
+    """Rotates the listed physical pages of k_pool in place by their deltas."""
+    if pages.numel() != deltas.numel():
+        raise ValueError("pages and deltas differ in length")
+    st = lib().seg_paged_attn_rope_align(
+        ctypes.byref(dims), _ptr(k_pool, torch.bfloat16, "k_pool"), _ptr(pages, torch.int32, "pages"),
+        _ptr(deltas, torch.int32, "deltas"), pages.numel(), float(rope_base), _stream(stream))
+    _check("seg_paged_attn_rope_align", st)
 
 
 def seg_paged_attn_validate(dims: spa_dims_t, ctx_lens, q_indptr, seg_table, page_table,

@@ -312,6 +312,29 @@ spa_status_t seg_paged_attn_page_summary(const spa_dims_t* dims, const void* k_p
   return hip_status(timed_launch("page_summary", s, [&] { return launch_page_summary(a, s); }));
 }
 
+spa_status_t seg_paged_attn_rope_align(const spa_dims_t* dims, void* k_pool, const int32_t* pages,
+                                       const int32_t* deltas, int64_t n, double rope_base,
+                                       void* stream) {
+  const spa_status_t st = check_dims(dims);
+  if (st != SPA_OK) return st;
+  if (n < 0 || n >= (int64_t(1) << 31) || !std::isfinite(rope_base) || rope_base <= 1.0)
+    return SPA_ERR_INVALID_ARG;
+  if (n > 0 && (k_pool == nullptr || pages == nullptr || deltas == nullptr)) return SPA_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(k_pool) & 15) return SPA_ERR_INVALID_ARG;
+  if (n == 0) return SPA_OK;
+  RopeArgs a{};
+  a.k_pool = static_cast<__bf16*>(k_pool);
+  a.pages = pages;
+  a.deltas = deltas;
+  a.n = n;
+  a.n_phys = dims->num_phys_pages;
+  a.D = dims->head_dim;
+  a.P = dims->page_size;
+  a.base = rope_base;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return hip_status(timed_launch("rope_align", s, [&] { return launch_rope_align(a, s); }));
+}
+
 spa_status_t seg_paged_attn_validate(const spa_dims_t* dims, const int32_t* ctx_lens,
                                      const int32_t* q_indptr, const int32_t* seg_table,
                                      const int32_t* page_table, const int32_t* sel_indptr,

@@ -38,6 +38,17 @@ struct FwdArgs {
   float scale_log2;           // softmax scale * log2(e)
 };
 
+// RoPE alignment of cached key pages.
+struct RopeArgs {
+  __bf16* k_pool;             // [n_phys, P*D], tile layout, rotated in place
+  const int32_t* pages;       // [n] physical page ids (outside [0, n_phys): skipped)
+  const int32_t* deltas;      // [n] p_on - p_off of each page's tokens
+  int64_t n;
+  int64_t n_phys;
+  int32_t D, P;
+  double base;                // theta_i = base^(-2 i / D)
+};
+
 // Page selection.
 struct SelArgs {
   const int32_t* ctx_lens;
@@ -83,6 +94,7 @@ constexpr int kSelectKeyCache = 4096;  // keys held in LDS by the select kernel
 constexpr int kSelectCand = 1024;      // radix-select candidate list in LDS
 
 hipError_t launch_decode(const FwdArgs& a, hipStream_t stream);
+hipError_t launch_rope_align(const RopeArgs& a, hipStream_t stream);
 hipError_t launch_combine(const FwdArgs& a, hipStream_t stream);
 int decode_blocks_per_cu(int D, int units);
 

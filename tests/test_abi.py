@@ -111,3 +111,17 @@ def test_validate_needs_workspace():
     st = L.seg_paged_attn_validate(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 100,
                                    None, None, None, 0, None)
     assert st == -3
+
+
+def test_bad_rope_align_args_rejected():
+    d = _dims()
+    L = B.lib()
+    assert L.seg_paged_attn_rope_align(ctypes.byref(d), FAKE, FAKE, FAKE, -1, 1e4, None) == -1
+    assert L.seg_paged_attn_rope_align(ctypes.byref(d), FAKE, FAKE, FAKE, 1 << 31, 1e4, None) == -1
+    assert L.seg_paged_attn_rope_align(ctypes.byref(d), FAKE, FAKE, FAKE, 4, 1.0, None) == -1
+    assert L.seg_paged_attn_rope_align(ctypes.byref(d), FAKE, FAKE, FAKE, 4, float("nan"), None) == -1
+    assert L.seg_paged_attn_rope_align(ctypes.byref(d), FAKE, None, FAKE, 4, 1e4, None) == -1
+    assert L.seg_paged_attn_rope_align(ctypes.byref(d), ctypes.c_void_p(0x1002), FAKE, FAKE, 4, 1e4,
+                                       None) == -1
+    # nothing to do: no launch, no pointer needed
+    assert L.seg_paged_attn_rope_align(ctypes.byref(d), None, None, None, 0, 1e4, None) == 0
