@@ -228,6 +228,69 @@ def cpu_baseline(cfg, wl, seconds=12.0, max_procs=16):
                       f"processes (host cores available: {cores})"}
 
 
+def bench_rope_align(args, wl):
+    """RoPE alignment (Section 4.2) of every key page of the workload's pool,
+    each page by a seeded shift: one read and one write of the K pool."""
+    import torch
+
+    from paper_2606_06256_amd import binding, build_lib
+    from paper_2606_06256_amd.device import DeviceWorkload
+    if not os.path.exists(binding.LIB_PATH):
+        build_lib.build()
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+    dw = DeviceWorkload(wl)
+    n = int(dw.k_pool.shape[0])
+    pages = torch.arange(n, dtype=torch.int32, device="cuda")
+    g = torch.Generator().manual_seed(7)
+    deltas = torch.randint(-131072, 131072, (n,), generator=g, dtype=torch.int32).cuda()
+    run = lambda: binding.seg_paged_attn_rope_align(dw.dims, dw.k_pool, pages, deltas, 10000.0)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        run()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    binding.profile_begin()
+    for _ in range(args.steps):
+        run()
+    torch.cuda.synchronize()
+    prof = binding.profile_end()
+    nl, tl = prof["rope_align"]
+    launch_ms = tl / nl
+    nbytes = 2 * n * wl.P * wl.D * 2          # every key page read and written once
+    gbs = nbytes / (launch_ms * 1e-3) / 1e9
+    # the same bytes moved by a plain device copy (read + write), for scale
+    src = dw.k_pool.view(-1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbs = nbytes / (c0.elapsed_time(c1) / args.steps * 1e-3) / 1e9
+    del dst
+    print(json.dumps({
+        "metric": "RoPE alignment of cached key pages: HBM GB/s", "value": round(nbytes / (ms * 1e-3) / 1e9, 1),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {"workload": wl.spec.name + " key pool", "pages": n, "page_size": wl.P, "head_dim": wl.D,
+                   "bytes_per_launch": nbytes, "device_copy_gbs_same_bytes": round(copy_gbs, 1)},
+        "roofline": {"kernel": "rope_align", "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "launch_ms": round(launch_ms, 5)},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -237,6 +300,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (scale for HBM byte counters)")
+    ap.add_argument("--op", choices=["step", "rope_align"], default="step",
+                    help="step: the hot path (default); rope_align: RoPE alignment of every "
+                         "key page of the workload's pool, timed on its own")
     ap.add_argument("--record-traffic", choices=sorted(KERNELS),
                     help="write the kernel's HBM traffic entry from rocprofv3 --pmc output dirs "
                          "(--fetch, --write, --calib-fetch, --calib-write); runs nothing on the GPU")
@@ -269,6 +335,9 @@ def main():
 
     from paper_2606_06256_amd import inputs as I
     wl = I.config(args.workload)
+    if args.op == "rope_align":
+        bench_rope_align(args, wl)
+        return
 
     # CPU baseline first, before anything initialises the GPU
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, wl)
