@@ -92,6 +92,12 @@ def test_refreshed_key_sums_equal_a_full_recompute():
     kn, vn = _new_tokens(30, wl.Hkv, wl.D, 4)
     k2, v2, touched = BO.append(kp, vp, wl.seg_table, wl.page_table, [50, 64], [0, 14, 30], kn, vn,
                                 wl.Hkv, wl.P, wl.pps)
+    assert any(v < wl.P for v in touched.values())   # a partial page is among them
+    # slots past a page's valid tokens hold anything (here 1.0): never summed
+    for ph, valid in touched.items():
+        kt = k2[ph].reshape(wl.P // 16, wl.D // 8, 16, 8)
+        for slot in range(valid, wl.P):
+            kt[slot // 16, :, slot % 16, :] = 0x3F80
     ksum0 = np.full((kp.shape[0], wl.D), np.float32(7.0))
     ks = BO.refresh_key_sums(ksum0, k2, touched, wl.P, wl.D)
     seg = wl.seg_table.reshape(wl.B * wl.Hkv, -1)
