@@ -188,6 +188,37 @@ spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int
                                 size_t workspace_bytes, void* stream);
 
 /*
+ * Appending tokens to the head-segmented KV pool (BuildState, Section 4.5,
+ * over the head segments of Section 4.3), with an optional refresh of the key
+ * sums of every page that received a token.
+ * Request r's new tokens new_indptr[r] .. new_indptr[r+1]-1 take positions
+ * ctx_lens[r], ctx_lens[r] + 1, ... of each KV head's stream; position t is
+ * slot t % P of logical page t / P, translated through seg_table and
+ * page_table as in Algorithm 2. A token whose segment is unmapped, or whose
+ * position lies past the segment table, is dropped. ctx_lens is read, not
+ * updated: the caller adds the appended counts.
+ * In:  ctx_lens device int32 [B] (tokens stored before the append);
+ *      new_indptr device int32 [B+1] (0, non-decreasing, new_indptr[B] = n_new);
+ *      k_new, v_new device bf16 [n_new, Hkv, D]; seg_table, page_table as for
+ *      seg_paged_attn_fwd.
+ * In/out: k_pool, v_pool device bf16 [num_phys_pages, P * D] (tile layout);
+ *      page_ksum device fp32 [num_phys_pages, D] or NULL: for each page that
+ *      received a token, the float32 rounding of the sum of its valid keys
+ *      (valid = min(P, new length - page start)), as seg_paged_attn_page_summary.
+ * A page written by this call must belong to one (request, KV head) only
+ * (segments shared between requests are read-only); two units writing one
+ * page is a data race.
+ * Errors: INVALID_ARG for n_new < 0, a null pointer needed for n_new > 0, or
+ * misaligned pools or page_ksum. Asynchronous on stream; n_new = 0 launches
+ * nothing.
+ */
+spa_status_t seg_paged_attn_append(const spa_dims_t* dims, const int32_t* ctx_lens,
+                                   const int32_t* new_indptr, const void* k_new, const void* v_new,
+                                   int64_t n_new, const int32_t* seg_table,
+                                   const int32_t* page_table, void* k_pool, void* v_pool,
+                                   float* page_ksum, void* stream);
+
+/*
  * RoPE positional alignment of cached keys (Section 4.2): a key cached at
  * offline position p_off and reused at online position p_on is replaced by
  * R(p_on) R(p_off)^-1 K(p_off), which is the rotation by delta = p_on - p_off.

@@ -66,6 +66,9 @@ def lib() -> ctypes.CDLL:
                                      ctypes.c_int64, _P, _P, _P, ctypes.c_size_t, _P]
     L.seg_paged_attn_page_summary.restype = ctypes.c_int
     L.seg_paged_attn_page_summary.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P]
+    L.seg_paged_attn_append.restype = ctypes.c_int
+    L.seg_paged_attn_append.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P, ctypes.c_int64,
+                                         _P, _P, _P, _P, _P, _P]
     L.seg_paged_attn_rope_align.restype = ctypes.c_int
     L.seg_paged_attn_rope_align.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, ctypes.c_int64,
                                              ctypes.c_double, _P]
@@ -165,6 +168,23 @@ def seg_paged_attn_page_summary(dims: spa_dims_t, k_pool, page_valid_tokens, pag
         _ptr(page_valid_tokens, torch.int32, "page_valid_tokens"),
         _ptr(page_ksum, torch.float32, "page_ksum"), _stream(stream))
     _check("seg_paged_attn_page_summary", st)
+
+
+def seg_paged_attn_append(dims: spa_dims_t, ctx_lens, new_indptr, k_new, v_new, seg_table, page_table,
+                          k_pool, v_pool, page_ksum=None, stream=None):
+    """Writes the new tokens' keys and values into their pages (and refreshes
+    the key sums of the pages written when page_ksum is given)."""
+    n_new = k_new.shape[0]
+    if v_new.shape != k_new.shape:
+        raise ValueError("k_new and v_new differ in shape")
+    st = lib().seg_paged_attn_append(
+        ctypes.byref(dims), _ptr(ctx_lens, torch.int32, "ctx_lens"),
+        _ptr(new_indptr, torch.int32, "new_indptr"), _ptr(k_new, torch.bfloat16, "k_new"),
+        _ptr(v_new, torch.bfloat16, "v_new"), n_new, _ptr(seg_table, torch.int32, "seg_table"),
+        _ptr(page_table, torch.int32, "page_table"), _ptr(k_pool, torch.bfloat16, "k_pool"),
+        _ptr(v_pool, torch.bfloat16, "v_pool"), _ptr(page_ksum, torch.float32, "page_ksum"),
+        _stream(stream))
+    _check("seg_paged_attn_append", st)
 
 
 def seg_paged_attn_rope_align(dims: spa_dims_t, k_pool, pages, deltas, rope_base: float = 10000.0,

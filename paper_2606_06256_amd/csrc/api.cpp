@@ -312,6 +312,46 @@ spa_status_t seg_paged_attn_page_summary(const spa_dims_t* dims, const void* k_p
   return hip_status(timed_launch("page_summary", s, [&] { return launch_page_summary(a, s); }));
 }
 
+spa_status_t seg_paged_attn_append(const spa_dims_t* dims, const int32_t* ctx_lens,
+                                   const int32_t* new_indptr, const void* k_new, const void* v_new,
+                                   int64_t n_new, const int32_t* seg_table,
+                                   const int32_t* page_table, void* k_pool, void* v_pool,
+                                   float* page_ksum, void* stream) {
+  const spa_status_t st = check_dims(dims);
+  if (st != SPA_OK) return st;
+  if (n_new < 0 || n_new * dims->num_kv_heads >= (int64_t(1) << 31) / 16) return SPA_ERR_INVALID_ARG;
+  if (n_new > 0 && (ctx_lens == nullptr || new_indptr == nullptr || k_new == nullptr ||
+                    v_new == nullptr || seg_table == nullptr || page_table == nullptr ||
+                    k_pool == nullptr || v_pool == nullptr))
+    return SPA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(k_pool) | reinterpret_cast<uintptr_t>(v_pool) |
+       reinterpret_cast<uintptr_t>(k_new) | reinterpret_cast<uintptr_t>(v_new) |
+       reinterpret_cast<uintptr_t>(page_ksum)) & 15)
+    return SPA_ERR_INVALID_ARG;
+  if (n_new == 0) return SPA_OK;
+  AppendArgs a{};
+  a.ctx_lens = ctx_lens;
+  a.new_indptr = new_indptr;
+  a.k_new = static_cast<const __bf16*>(k_new);
+  a.v_new = static_cast<const __bf16*>(v_new);
+  a.seg_table = seg_table;
+  a.page_table = page_table;
+  a.k_pool = static_cast<__bf16*>(k_pool);
+  a.v_pool = static_cast<__bf16*>(v_pool);
+  a.page_ksum = page_ksum;
+  a.n_new = n_new;
+  a.n_virtual = dims->num_virtual_pages;
+  a.n_phys = dims->num_phys_pages;
+  a.B = dims->num_requests;
+  a.Hkv = dims->num_kv_heads;
+  a.D = dims->head_dim;
+  a.P = dims->page_size;
+  a.pps = dims->pages_per_segment;
+  a.max_segs = dims->max_segments;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return hip_status(timed_launch("append", s, [&] { return launch_append(a, s); }));
+}
+
 spa_status_t seg_paged_attn_rope_align(const spa_dims_t* dims, void* k_pool, const int32_t* pages,
                                        const int32_t* deltas, int64_t n, double rope_base,
                                        void* stream) {

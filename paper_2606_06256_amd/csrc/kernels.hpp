@@ -49,6 +49,21 @@ struct RopeArgs {
   double base;                // theta_i = base^(-2 i / D)
 };
 
+// Appending tokens to their pages (and refreshing page key sums).
+struct AppendArgs {
+  const int32_t* ctx_lens;    // [B] tokens stored before the append
+  const int32_t* new_indptr;  // [B+1]
+  const __bf16* k_new;        // [n_new, Hkv, D]
+  const __bf16* v_new;
+  const int32_t* seg_table;
+  const int32_t* page_table;
+  __bf16* k_pool;
+  __bf16* v_pool;
+  float* page_ksum;           // [n_phys, D] or null
+  int64_t n_new, n_virtual, n_phys;
+  int32_t B, Hkv, D, P, pps, max_segs;
+};
+
 // Page selection.
 struct SelArgs {
   const int32_t* ctx_lens;
@@ -95,6 +110,7 @@ constexpr int kSelectCand = 1024;      // radix-select candidate list in LDS
 
 hipError_t launch_decode(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_rope_align(const RopeArgs& a, hipStream_t stream);
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_combine(const FwdArgs& a, hipStream_t stream);
 int decode_blocks_per_cu(int D, int units);
 

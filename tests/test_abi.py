@@ -125,3 +125,19 @@ def test_bad_rope_align_args_rejected():
                                        None) == -1
     # nothing to do: no launch, no pointer needed
     assert L.seg_paged_attn_rope_align(ctypes.byref(d), None, None, None, 0, 1e4, None) == 0
+
+
+def test_bad_append_args_rejected():
+    d = _dims()
+    L = B.lib()
+    f = lambda **kw: L.seg_paged_attn_append(
+        ctypes.byref(d), kw.get("ctx", FAKE), kw.get("ind", FAKE), kw.get("kn", FAKE), kw.get("vn", FAKE),
+        kw.get("n", 4), FAKE, FAKE, kw.get("kp", FAKE), FAKE, kw.get("ks", None), None)
+    assert f(n=-1) == -1
+    assert f(ctx=None) == -1
+    assert f(kn=None) == -1
+    assert f(kp=ctypes.c_void_p(0x1008)) == -1
+    assert f(ks=ctypes.c_void_p(0x1004)) == -1
+    # nothing to append: no launch, no pointer needed
+    assert L.seg_paged_attn_append(ctypes.byref(d), None, None, None, None, 0, None, None, None, None,
+                                   None, None) == 0
