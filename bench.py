@@ -291,6 +291,66 @@ def bench_rope_align(args, wl):
     }), flush=True)
 
 
+def bench_append(args, wl):
+    """Appending each request's n_q new tokens (the workload's query chunk, at
+    the end of its context) into their pages, with the key-sum refresh of
+    every page written."""
+    import torch
+
+    from paper_2606_06256_amd import binding, build_lib
+    from paper_2606_06256_amd.device import DeviceWorkload
+    if not os.path.exists(binding.LIB_PATH):
+        build_lib.build()
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+    dw = DeviceWorkload(wl)
+    nq = np.diff(wl.q_indptr).astype(np.int64)
+    L0 = (wl.ctx_lens - nq).astype(np.int32)
+    n_new = int(nq.sum())
+    g = torch.Generator().manual_seed(11)
+    kn = torch.randn(n_new, wl.Hkv, wl.D, generator=g).to(torch.bfloat16).cuda()
+    vn = torch.randn(n_new, wl.Hkv, wl.D, generator=g).to(torch.bfloat16).cuda()
+    ks = torch.zeros(wl.num_phys, wl.D, dtype=torch.float32, device="cuda")
+    l0 = torch.from_numpy(L0).cuda()
+    ind = torch.from_numpy(wl.q_indptr.astype(np.int32)).cuda()
+    run = lambda: binding.seg_paged_attn_append(dw.dims, l0, ind, kn, vn, dw.seg_table, dw.page_table,
+                                                dw.k_pool, dw.v_pool, ks)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        run()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    # bytes: new K and V read and written; every written page's valid keys
+    # read back for its sum, and the sum written
+    touched_tokens = 0
+    touched_pages = 0
+    for r in range(wl.B):
+        if nq[r] == 0:
+            continue
+        j0, j1 = int(L0[r]) // wl.P, (int(wl.ctx_lens[r]) - 1) // wl.P
+        for j in range(j0, j1 + 1):
+            touched_pages += wl.Hkv
+            touched_tokens += wl.Hkv * min(wl.P, int(wl.ctx_lens[r]) - j * wl.P)
+    nbytes = 4 * n_new * wl.Hkv * wl.D * 2 + touched_tokens * wl.D * 2 + touched_pages * wl.D * 4
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "KV append with key-sum refresh: HBM GB/s", "value": round(gbs, 1), "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.spec.name + " chunk append", "new_tokens": n_new, "kv_heads": wl.Hkv,
+                   "pages_touched": touched_pages, "bytes_per_call": nbytes},
+        "roofline": {"kernel": "append + key_refresh", "bound": "hbm", "achieved": round(gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -300,9 +360,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (scale for HBM byte counters)")
-    ap.add_argument("--op", choices=["step", "rope_align"], default="step",
+    ap.add_argument("--op", choices=["step", "rope_align", "append"], default="step",
                     help="step: the hot path (default); rope_align: RoPE alignment of every "
-                         "key page of the workload's pool, timed on its own")
+                         "key page of the workload's pool; append: writing each request's "
+                         "query chunk of new tokens into its pages with the key-sum refresh")
     ap.add_argument("--record-traffic", choices=sorted(KERNELS),
                     help="write the kernel's HBM traffic entry from rocprofv3 --pmc output dirs "
                          "(--fetch, --write, --calib-fetch, --calib-write); runs nothing on the GPU")
@@ -337,6 +398,9 @@ def main():
     wl = I.config(args.workload)
     if args.op == "rope_align":
         bench_rope_align(args, wl)
+        return
+    if args.op == "append":
+        bench_append(args, wl)
         return
 
     # CPU baseline first, before anything initialises the GPU

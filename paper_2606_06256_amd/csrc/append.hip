@@ -9,27 +9,29 @@
 // dropped. A refreshed key sum is the float32 rounding of the exact sum of the
 // page's valid keys (accumulated in float64), as the page summary kernel.
 //
-// append_kernel: D/8 lanes per (token, KV head); lane c writes K chunk c (16
-// bytes at ((c * 16 + u) * 8) of the slot's tile) and the 8 V entries of
-// dimensions 8c .. 8c + 7 (2 bytes each, 32 bytes apart in the [D][16] tile).
-// Different tokens write different bytes, so no two lanes touch the same one.
-// key_refresh_kernel: one block per unit, its touched pages in turn, one
+// append_kernel: a block takes 16 consecutive new tokens of one KV head and
+// all D/8 chunks; lane = token + 16 * chunk, so each store instruction writes
+// 16 consecutive K slots (16 bytes each) or, per dimension, 16 consecutive V
+// entries (32 bytes) of a [D][16] tile. Different tokens write different
+// bytes, so no two lanes touch the same one.
+// key_refresh_kernel: blocks (unit, round) over the unit's touched pages, one
 // thread per (page, 8-dimension chunk).
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace segpa {
 
+// Token group of 16 consecutive new tokens x all chunks of one KV head per
+// block: lane = token + 16 * chunk-in-round, so for each chunk the 16 tokens
+// of a tile write 16 consecutive K slots and, per dimension, 16 consecutive
+// V entries (32 bytes).
 __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
   const int D = a.D;
   const int P = a.P;
   const int CH = D / 8;
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t pair = gid / CH;               // (token, KV head)
-  const int c = (int)(gid - pair * CH);
-  if (pair >= a.n_new * a.Hkv) return;
-  const int64_t i = pair / a.Hkv;
-  const int g = (int)(pair - i * a.Hkv);
+  const int64_t i = (int64_t)blockIdx.x * kTile + (threadIdx.x & (kTile - 1));
+  const int g = blockIdx.y;
+  if (i >= a.n_new) return;
   // request of token i: last r with new_indptr[r] <= i
   int lo = 0, hi = a.B - 1;
   while (lo < hi) {
@@ -47,15 +49,20 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
   if (ph < 0) return;
   const int t = slot >> 4, u = slot & (kTile - 1);
   const int64_t tile = (int64_t)ph * P * D + (int64_t)t * kTile * D;
-  const int64_t src = (i * a.Hkv + g) * D + c * 8;
-  *reinterpret_cast<s16x8*>(a.k_pool + tile + (c * kTile + u) * 8) =
-      *reinterpret_cast<const s16x8*>(a.k_new + src);
-  const s16x8 v = *reinterpret_cast<const s16x8*>(a.v_new + src);
   unsigned short* vt = reinterpret_cast<unsigned short*>(a.v_pool + tile);
+  for (int c = threadIdx.x >> 4; c < CH; c += blockDim.x >> 4) {
+    const int64_t src = (i * a.Hkv + g) * D + c * 8;
+    *reinterpret_cast<s16x8*>(a.k_pool + tile + (c * kTile + u) * 8) =
+        *reinterpret_cast<const s16x8*>(a.k_new + src);
+    const s16x8 v = *reinterpret_cast<const s16x8*>(a.v_new + src);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) vt[(c * 8 + e) * kTile + u] = (unsigned short)v[e];
+    for (int e = 0; e < 8; ++e) vt[(c * 8 + e) * kTile + u] = (unsigned short)v[e];
+  }
 }
 
+// Grid (unit, page round): thread (page slot, chunk) of each round of
+// 256 / (D/8) pages of the unit's touched range; a tile's 16 keys are loaded
+// before they are added.
 __global__ __launch_bounds__(256) void key_refresh_kernel(const AppendArgs a) {
   const int u_id = blockIdx.x;                 // unit (r, g)
   const int r = u_id / a.Hkv;
@@ -71,21 +78,27 @@ __global__ __launch_bounds__(256) void key_refresh_kernel(const AppendArgs a) {
   const int j0 = (int)(L0 / P);
   const int j1 = (int)((min(L1, max_tokens) - 1) / P);
   const int32_t* seg_row = a.seg_table + (int64_t)u_id * a.max_segs;
-  const int per = blockDim.x / CH;             // pages per round
-  for (int jb = j0; jb <= j1; jb += per) {
-    const int j = jb + threadIdx.x / CH;
-    const int c = threadIdx.x % CH;
-    if (threadIdx.x >= per * CH || j > j1) continue;
+  const int per = blockDim.x / CH;             // pages per block round
+  const int c = threadIdx.x % CH;
+  if (threadIdx.x >= per * CH) return;
+  for (int j = j0 + (int)blockIdx.y * per + (int)threadIdx.x / CH; j <= j1; j += (int)gridDim.y * per) {
     const int ph = translate_page(seg_row, a.page_table, j, a.pps, a.max_segs, a.n_virtual, a.n_phys);
     if (ph < 0) continue;
     const int valid = (int)min<int64_t>(P, L1 - (int64_t)j * P);
     const __bf16* base = a.k_pool + (int64_t)ph * P * D;
     double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int tok = 0; tok < valid; ++tok) {
-      const s16x8 x = *reinterpret_cast<const s16x8*>(base + (int64_t)(tok >> 4) * kTile * D +
-                                                      (c * kTile + (tok & (kTile - 1))) * 8);
+    for (int t = 0; t * kTile < valid; ++t) {
+      s16x8 x[kTile];
+      const __bf16* tp = base + (int64_t)t * kTile * D + c * kTile * 8;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += (double)bf16_bits_to_float((uint16_t)x[e]);
+      for (int uu = 0; uu < kTile; ++uu) x[uu] = *reinterpret_cast<const s16x8*>(tp + uu * 8);
+#pragma unroll
+      for (int uu = 0; uu < kTile; ++uu) {
+        if (t * kTile + uu < valid) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[e] += (double)bf16_bits_to_float((uint16_t)x[uu][e]);
+        }
+      }
     }
     float* o = a.page_ksum + (int64_t)ph * D + c * 8;
     *reinterpret_cast<float4*>(o) = make_float4((float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]);
@@ -94,14 +107,12 @@ __global__ __launch_bounds__(256) void key_refresh_kernel(const AppendArgs a) {
 }
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
-  const int64_t threads = a.n_new * a.Hkv * (a.D / 8);
-  if (threads > 0) {
-    const int64_t blocks = (threads + 255) / 256;
-    hipLaunchKernelGGL(append_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess || a.page_ksum == nullptr) return e;
-    hipLaunchKernelGGL(key_refresh_kernel, dim3((unsigned)(a.B * a.Hkv)), dim3(256), 0, stream, a);
-  }
+  if (a.n_new <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((a.n_new + kTile - 1) / kTile), (unsigned)a.Hkv);
+  hipLaunchKernelGGL(append_kernel, grid, dim3(256), 0, stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.page_ksum == nullptr) return e;
+  hipLaunchKernelGGL(key_refresh_kernel, dim3((unsigned)(a.B * a.Hkv), 8), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
