@@ -56,6 +56,37 @@ def unit_chunk_mass(q: np.ndarray, K: np.ndarray, pages: Sequence[int], P: int, 
     return m
 
 
+def chunk_token_mass(q: np.ndarray, K: np.ndarray, pages: Sequence[int], P: int, scale: float,
+                     k: int) -> float:
+    """Mass of chunk token k alone (same definition as unit_chunk_mass), for
+    sampling long chunks: only the rows i >= k are visited."""
+    n_q, G, _ = q.shape
+    L = K.shape[0]
+    tok = S.selected_tokens(pages, L, P)
+    pos = L - n_q + k
+    if pos < 0 or pos not in set(tok.tolist()):
+        return 0.0
+    KT = K[tok]
+    at = int(np.searchsorted(tok, pos))
+    total = 0.0
+    for i in range(k, n_q):
+        n_i = int(np.searchsorted(tok, L - n_q + i, side="right"))   # keys at or before query i
+        s = scale * (KT[:n_i] @ q[i].T)                # [n_i, G]
+        e = np.exp(s - s.max(axis=0))
+        total += float(np.sum(e[at] / e.sum(axis=0)))
+    return total
+
+
+def columns_to_token_mass(cols: np.ndarray) -> np.ndarray:
+    """Token masses from per-column masses [n, c]: the float32 sum of a row's
+    columns in column order; a sum that is negative or NaN counts as 0."""
+    cols = np.asarray(cols, dtype=np.float32)
+    m = np.zeros(cols.shape[0], dtype=np.float32)
+    for c in range(cols.shape[1]):
+        m = (m + cols[:, c]).astype(np.float32)
+    return np.where(m >= 0, m, np.float32(0)).astype(np.float32)
+
+
 def select_tokens(mass: np.ndarray, tau: float, recent: int) -> np.ndarray:
     """Kept positions (ascending) of one request's chunk given its token masses."""
     n = mass.size

@@ -62,3 +62,33 @@ def test_ties_go_to_the_earlier_token_and_recent_tokens_are_kept():
     np.testing.assert_array_equal(M.select_tokens(np.zeros(4), 0.5, 1), [3])
     assert M.mass_cover_fraction(np.array([8.0, 1.0, 0.5, 0.5])) == 1.0
     assert M.mass_cover_fraction(np.array([99.0, 1.0, 0.0, 0.0]), 0.99) == 0.25
+
+
+def test_single_token_mass_equals_dense_column_sum():
+    rng = np.random.default_rng(3)
+    L, n_q, G, D, P = 50, 20, 2, 8, 8
+    K = rng.standard_normal((L, D))
+    q = rng.standard_normal((n_q, G, D))
+    pages = [0, 2, 4, 6]                               # chunk tokens 30..49: page 5 (40..47) missing
+    s = torch.einsum("igd,td->igt", torch.from_numpy(q), torch.from_numpy(K)) * 0.4
+    pos = torch.arange(L)
+    sel = torch.zeros(L, dtype=torch.bool)
+    for p in pages:
+        sel[p * P:(p + 1) * P] = True
+    mask = (pos[None, None, :] <= (L - n_q + torch.arange(n_q))[:, None, None]) & sel[None, None, :]
+    w = torch.softmax(s.masked_fill(~mask, float("-inf")), dim=-1)
+    want = w.sum(dim=(0, 1))[L - n_q:].numpy()
+    for k in range(n_q):
+        assert abs(M.chunk_token_mass(q, K, pages, P, 0.4, k) - want[k]) < 1e-12, k
+    np.testing.assert_allclose(M.unit_chunk_mass(q, K, pages, P, 0.4), want, rtol=1e-12, atol=1e-14)
+    assert all(want[k] == 0 for k in range(n_q) if not sel[L - n_q + k])
+
+
+def test_columns_to_token_mass_float32_order_and_sanitising():
+    cols = np.array([[1.0, 2.0, 3.0], [2.0 ** 24, 1.0, 1.0], [-5.0, 1.0, 1.0], [np.nan, 1.0, 0.0],
+                     [-0.0, -0.0, -0.0]], dtype=np.float32)
+    m = M.columns_to_token_mass(cols)
+    assert m.dtype == np.float32
+    # 2^24 + 1 rounds back to 2^24 in float32 at each step (column order), not 2^24 + 2
+    np.testing.assert_array_equal(m, np.array([6.0, 2.0 ** 24, 0.0, 0.0, 0.0], dtype=np.float32))
+    assert not np.signbit(m[4])
