@@ -351,19 +351,97 @@ def bench_append(args, wl):
     }), flush=True)
 
 
+def bench_token_mass(args, wl, tau=0.2, recent=128):
+    """The attention-mass token selection after a chunked-prefill forward:
+    the probability pass (token_mass) and the per-request selection
+    (select_tokens), at the sparse-FFN setting the paper gives for Qwen3-32B
+    (mass threshold 0.2, the most recent 128 tokens always kept)."""
+    import torch
+
+    from paper_2606_06256_amd import binding, build_lib
+    from paper_2606_06256_amd.device import DeviceWorkload
+    if not os.path.exists(binding.LIB_PATH):
+        build_lib.build()
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+    dw = DeviceWorkload(wl)
+    if wl.spec.sel_mode == 3:
+        dw.summary()
+    dw.select()
+    dw.fwd()                                  # the lse the masses are normalised by
+
+    def run():
+        dw.token_mass()
+        dw.select_tokens(tau, recent)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        run()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    binding.profile_begin()
+    for _ in range(args.steps):
+        run()
+    torch.cuda.synchronize()
+    prof = binding.profile_end()
+    n_m, t_m = prof["token_mass"]
+    n_s, t_s = prof["select_tokens"]
+    mass_ms, sel_ms = t_m / n_m, t_s / n_s
+    # algorithmic bytes of token_mass: every chunk row of q and its lse read
+    # once, the chunk's selected keys read once, the masses written; flops:
+    # 2 D per visible (row, chunk key) pair
+    ind, pages = dw.selection()
+    nq = np.diff(wl.q_indptr).astype(np.int64)
+    chunk_keys, pairs = 0, 0
+    for u in range(wl.num_units):
+        r = u // wl.Hkv
+        L, n = int(wl.ctx_lens[r]), int(nq[r])
+        pg = set(pages[ind[u]:ind[u + 1]].tolist())
+        ks = [k for k in range(n) if (L - n + k) >= 0 and (L - n + k) // wl.P in pg]
+        chunk_keys += len(ks)
+        pairs += wl.G * sum(n - k for k in ks)
+    abytes = wl.total_q * wl.Hq * (wl.D * 2 + 4) + chunk_keys * wl.D * 2 + wl.total_q * wl.Hkv * 4
+    flops = 2 * wl.D * pairs
+    gbs = abytes / (mass_ms * 1e-3) / 1e9
+    tfs = flops / (mass_ms * 1e-3) / 1e12
+    keep_frac = float(dw.keep_count.sum().item()) / max(1, wl.total_q)
+    print(json.dumps({
+        "metric": "attention-mass token selection: chunk tokens/s", "value": round(wl.total_q / (ms * 1e-3), 1),
+        "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.spec.name + " token selection", "chunk_tokens": wl.total_q,
+                   "q_heads": wl.Hq, "kv_heads": wl.Hkv, "tau": tau, "recent": recent,
+                   "kept_fraction": round(keep_frac, 4), "token_mass_ms": round(mass_ms, 5),
+                   "select_tokens_ms": round(sel_ms, 5), "token_mass_tflops": round(tfs, 2),
+                   "token_mass_mfma_frac": round(tfs / MFMA_BF16_PEAK_TFLOPS, 4)},
+        "roofline": {"kernel": "token_mass", "bound": "hbm", "achieved": round(gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": abytes, "flops_per_launch": flops,
+                     "launch_ms": round(mass_ms, 5)},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (default 2)")
+    ap.add_argument("--workload", type=int, default=None,
+                    help="named workload 1..9 (default 2; 9 for --op token_mass)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (scale for HBM byte counters)")
-    ap.add_argument("--op", choices=["step", "rope_align", "append"], default="step",
+    ap.add_argument("--op", choices=["step", "rope_align", "append", "token_mass"], default="step",
                     help="step: the hot path (default); rope_align: RoPE alignment of every "
                          "key page of the workload's pool; append: writing each request's "
-                         "query chunk of new tokens into its pages with the key-sum refresh")
+                         "query chunk of new tokens into its pages with the key-sum refresh; "
+                         "token_mass: attention-mass token selection after a chunked prefill")
     ap.add_argument("--record-traffic", choices=sorted(KERNELS),
                     help="write the kernel's HBM traffic entry from rocprofv3 --pmc output dirs "
                          "(--fetch, --write, --calib-fetch, --calib-write); runs nothing on the GPU")
@@ -372,6 +450,8 @@ def main():
     ap.add_argument("--calib-fetch")
     ap.add_argument("--calib-write")
     args = ap.parse_args()
+    if args.workload is None:
+        args.workload = 9 if args.op == "token_mass" else 2
     if args.record_traffic:
         args.kernel = args.record_traffic
         write_traffic_entry(args)
@@ -401,6 +481,9 @@ def main():
         return
     if args.op == "append":
         bench_append(args, wl)
+        return
+    if args.op == "token_mass":
+        bench_token_mass(args, wl)
         return
 
     # CPU baseline first, before anything initialises the GPU

@@ -252,6 +252,70 @@ spa_status_t seg_paged_attn_page_summary(const spa_dims_t* dims, const void* k_p
                                          void* stream);
 
 /*
+ * Attention mass of the chunk tokens (the probability pass feeding
+ * SelectImportantTokens, Algorithm 1; the token-importance signal of the
+ * sparse FFN, Section 4.5). For token t of request r's query chunk (query
+ * position L_r - n_q(r) + t) and KV head g:
+ *   mass[q_indptr[r] + t][g] = sum over query heads h of group g and chunk
+ *     queries i >= t of exp(scale * q[i][h] . k_t - lse[i][h]),
+ * where token t counts only if its logical page is in unit (r, g)'s selected
+ * list (as for seg_paged_attn_fwd: the same softmax, normalised by the
+ * forward's lse, so with the fwd's lse each row's weights over its attended
+ * keys sum to 1). A token whose page is not selected, unmapped, or whose
+ * position is negative has mass 0 for that head. A row whose lse is not
+ * finite contributes nothing. bf16 products, fp32 accumulation in a fixed
+ * order (results are reproducible bit for bit).
+ * In:  q, q_indptr, ctx_lens, k_pool, seg_table, page_table, sel_indptr,
+ *      sel_pages, sel_capacity as for seg_paged_attn_fwd (v_pool is not read);
+ *      lse device fp32 [total_q, Hq] from seg_paged_attn_fwd over the same
+ *      selected pages (natural log).
+ * Out: mass device fp32 [total_q, Hkv]. Rows outside every request's chunk
+ *      are not written.
+ * Errors: INVALID_ARG for a null pointer, q or k_pool not 16-byte aligned,
+ * lse or mass not 4-byte aligned. Asynchronous on stream; total_q = 0
+ * launches nothing.
+ */
+spa_status_t seg_paged_attn_token_mass(const spa_dims_t* dims, const void* q,
+                                       const int32_t* q_indptr, const int32_t* ctx_lens,
+                                       const void* k_pool, const int32_t* seg_table,
+                                       const int32_t* page_table, const int32_t* sel_indptr,
+                                       const int32_t* sel_pages, int64_t sel_capacity,
+                                       const float* lse, float* mass, void* stream);
+
+/*
+ * SelectImportantTokens (Algorithm 1) by cumulative attention mass (Section
+ * 4.5): per request, the smallest set of chunk tokens whose mass reaches tau
+ * of the chunk's total, together with the most recent `recent` tokens (the
+ * keep-recent-N rule of the sparse-FFN settings, Section 5).
+ * Token mass m_t = float32 sum of mass[q_indptr[r] + t][0 .. mass_cols-1] in
+ * column order (mass_cols = Hkv for the output of seg_paged_attn_token_mass,
+ * 1 for per-token masses); a sum that is negative or NaN counts as 0.
+ * Tokens are ranked by m_t descending, equal masses by position ascending;
+ * with M_k the float64 sum of the masses ranked before token k and T the
+ * float64 total, token k is kept iff T > 0 and M_k < tau * T (the ranked
+ * prefix that first reaches tau * T). Tokens t >= n_q(r) - recent are kept
+ * as well. The sums are formed in a parallel order: a result can differ from
+ * a sequential summation only where a partial sum lies within float64
+ * rounding of tau * T.
+ * In:  q_indptr device [B+1]; mass device fp32 [total_q, mass_cols]
+ *      (1 <= mass_cols <= 4096); 0 < tau <= 1; recent >= 0.
+ * Out: keep device uint8 [total_q] (1 kept, 0 not); kept device int32
+ *      [total_q] or NULL: the kept rows (absolute row ids) of request r in
+ *      ascending order at kept[q_indptr[r] ..], keep_count[r] of them (later
+ *      entries untouched); keep_count device int32 [B]; token_mass device fp32
+ *      [total_q] or NULL: m_t.
+ * Requires max_q_len <= 16384 (else UNSUPPORTED): a request's chunk is
+ * sorted in one workgroup's LDS. The 99%-mass fraction of a chunk is
+ * keep_count / n_q with tau = 0.99 and recent = 0.
+ * Errors: INVALID_ARG for a null required pointer, tau outside (0, 1],
+ * recent < 0, mass_cols outside [1, 4096], misaligned 4-byte outputs.
+ */
+spa_status_t seg_paged_attn_select_tokens(const spa_dims_t* dims, const int32_t* q_indptr,
+                                          const float* mass, int32_t mass_cols, double tau,
+                                          int32_t recent, uint8_t* keep, int32_t* kept,
+                                          int32_t* keep_count, float* token_mass, void* stream);
+
+/*
  * Synchronous check of table and list contents (debug aid). Checks q_indptr
  * (monotone, n_q <= min(max_q_len, L)), ctx_lens (0 <= L <= max_segments*pps*P),
  * sel_indptr (starts at 0, monotone), every selected page (in [0, n_pages),

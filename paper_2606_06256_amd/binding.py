@@ -72,6 +72,12 @@ def lib() -> ctypes.CDLL:
     L.seg_paged_attn_rope_align.restype = ctypes.c_int
     L.seg_paged_attn_rope_align.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, ctypes.c_int64,
                                              ctypes.c_double, _P]
+    L.seg_paged_attn_token_mass.restype = ctypes.c_int
+    L.seg_paged_attn_token_mass.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P, _P, _P, _P,
+                                            _P, ctypes.c_int64, _P, _P, _P]
+    L.seg_paged_attn_select_tokens.restype = ctypes.c_int
+    L.seg_paged_attn_select_tokens.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, ctypes.c_int32,
+                                               ctypes.c_double, ctypes.c_int32, _P, _P, _P, _P, _P]
     L.seg_paged_attn_validate.restype = ctypes.c_int
     L.seg_paged_attn_validate.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P, _P, _P,
                                           ctypes.c_int64, ctypes.POINTER(ctypes.c_int32),
@@ -196,6 +202,32 @@ def seg_paged_attn_rope_align(dims: spa_dims_t, k_pool, pages, deltas, rope_base
         ctypes.byref(dims), _ptr(k_pool, torch.bfloat16, "k_pool"), _ptr(pages, torch.int32, "pages"),
         _ptr(deltas, torch.int32, "deltas"), pages.numel(), float(rope_base), _stream(stream))
     _check("seg_paged_attn_rope_align", st)
+
+
+def seg_paged_attn_token_mass(dims: spa_dims_t, q, q_indptr, ctx_lens, k_pool, seg_table, page_table,
+                              sel_indptr, sel_pages, lse, mass, stream=None):
+    """mass [total_q, Hkv]: softmax mass each chunk token receives per KV head."""
+    st = lib().seg_paged_attn_token_mass(
+        ctypes.byref(dims), _ptr(q, torch.bfloat16, "q"), _ptr(q_indptr, torch.int32, "q_indptr"),
+        _ptr(ctx_lens, torch.int32, "ctx_lens"), _ptr(k_pool, torch.bfloat16, "k_pool"),
+        _ptr(seg_table, torch.int32, "seg_table"), _ptr(page_table, torch.int32, "page_table"),
+        _ptr(sel_indptr, torch.int32, "sel_indptr"), _ptr(sel_pages, torch.int32, "sel_pages"),
+        sel_pages.numel(), _ptr(lse, torch.float32, "lse"), _ptr(mass, torch.float32, "mass"),
+        _stream(stream))
+    _check("seg_paged_attn_token_mass", st)
+
+
+def seg_paged_attn_select_tokens(dims: spa_dims_t, q_indptr, mass, tau: float, recent: int, keep,
+                                 keep_count, kept=None, token_mass=None, stream=None):
+    """Per request: tokens of the smallest mass-ranked set reaching tau of the
+    total, plus the last `recent` tokens (keep mask, kept rows, counts)."""
+    cols = 1 if mass.dim() == 1 else mass.shape[1]
+    st = lib().seg_paged_attn_select_tokens(
+        ctypes.byref(dims), _ptr(q_indptr, torch.int32, "q_indptr"), _ptr(mass, torch.float32, "mass"),
+        cols, float(tau), int(recent), _ptr(keep, torch.uint8, "keep"), _ptr(kept, torch.int32, "kept"),
+        _ptr(keep_count, torch.int32, "keep_count"), _ptr(token_mass, torch.float32, "token_mass"),
+        _stream(stream))
+    _check("seg_paged_attn_select_tokens", st)
 
 
 def seg_paged_attn_validate(dims: spa_dims_t, ctx_lens, q_indptr, seg_table, page_table,

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsegpa.so")
 
-SOURCES = ["api.cpp", "append.hip", "decode.hip", "prefill.hip", "rope.hip", "select.hip", "summary.hip"]
+SOURCES = ["api.cpp", "append.hip", "decode.hip", "mass.hip", "prefill.hip", "rope.hip", "select.hip", "summary.hip"]
 ARCH = "gfx950"
 
 

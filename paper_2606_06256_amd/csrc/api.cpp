@@ -375,6 +375,88 @@ spa_status_t seg_paged_attn_rope_align(const spa_dims_t* dims, void* k_pool, con
   return hip_status(timed_launch("rope_align", s, [&] { return launch_rope_align(a, s); }));
 }
 
+spa_status_t seg_paged_attn_token_mass(const spa_dims_t* dims, const void* q,
+                                       const int32_t* q_indptr, const int32_t* ctx_lens,
+                                       const void* k_pool, const int32_t* seg_table,
+                                       const int32_t* page_table, const int32_t* sel_indptr,
+                                       const int32_t* sel_pages, int64_t sel_capacity,
+                                       const float* lse, float* mass, void* stream) {
+  const spa_status_t st = check_dims(dims);
+  if (st != SPA_OK) return st;
+  if (q == nullptr || q_indptr == nullptr || ctx_lens == nullptr || k_pool == nullptr ||
+      seg_table == nullptr || page_table == nullptr || sel_indptr == nullptr ||
+      sel_pages == nullptr || lse == nullptr || mass == nullptr || sel_capacity < 0 ||
+      sel_capacity >= (int64_t(1) << 31))
+    return SPA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(k_pool) | reinterpret_cast<uintptr_t>(q)) & 15)
+    return SPA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(lse) | reinterpret_cast<uintptr_t>(mass)) & 3)
+    return SPA_ERR_INVALID_ARG;
+  if (dims->total_q == 0) return SPA_OK;
+  MassArgs a{};
+  a.q = static_cast<const __bf16*>(q);
+  a.q_indptr = q_indptr;
+  a.ctx_lens = ctx_lens;
+  a.k_pool = static_cast<const __bf16*>(k_pool);
+  a.seg_table = seg_table;
+  a.page_table = page_table;
+  a.sel_indptr = sel_indptr;
+  a.sel_pages = sel_pages;
+  a.lse = lse;
+  a.mass = mass;
+  a.n_virtual = dims->num_virtual_pages;
+  a.n_phys = dims->num_phys_pages;
+  a.sel_capacity = sel_capacity;
+  a.B = dims->num_requests;
+  a.Hq = dims->num_q_heads;
+  a.Hkv = dims->num_kv_heads;
+  a.G = dims->num_q_heads / dims->num_kv_heads;
+  a.D = dims->head_dim;
+  a.P = dims->page_size;
+  a.pps = dims->pages_per_segment;
+  a.max_segs = dims->max_segments;
+  a.max_q_len = dims->max_q_len;
+  a.total_q = dims->total_q;
+  a.key_groups = (dims->max_q_len + token_mass_keys_per_block() - 1) / token_mass_keys_per_block();
+  const float scale = dims->softmax_scale > 0.f ? dims->softmax_scale
+                                                : 1.0f / std::sqrt((float)dims->head_dim);
+  a.scale_log2 = scale * kLog2e;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return hip_status(timed_launch("token_mass", s, [&] { return launch_token_mass(a, s); }));
+}
+
+spa_status_t seg_paged_attn_select_tokens(const spa_dims_t* dims, const int32_t* q_indptr,
+                                          const float* mass, int32_t mass_cols, double tau,
+                                          int32_t recent, uint8_t* keep, int32_t* kept,
+                                          int32_t* keep_count, float* token_mass, void* stream) {
+  const spa_status_t st = check_dims(dims);
+  if (st != SPA_OK) return st;
+  if (q_indptr == nullptr || keep_count == nullptr || mass_cols < 1 || mass_cols > 4096 ||
+      !(tau > 0.0 && tau <= 1.0) || recent < 0)
+    return SPA_ERR_INVALID_ARG;
+  if (dims->total_q > 0 && (mass == nullptr || keep == nullptr)) return SPA_ERR_INVALID_ARG;
+  if ((int64_t)dims->total_q * mass_cols >= (int64_t(1) << 31)) return SPA_ERR_UNSUPPORTED;
+  if (dims->max_q_len > kTokSelMax) return SPA_ERR_UNSUPPORTED;
+  if ((reinterpret_cast<uintptr_t>(mass) | reinterpret_cast<uintptr_t>(kept) |
+       reinterpret_cast<uintptr_t>(keep_count) | reinterpret_cast<uintptr_t>(token_mass)) & 3)
+    return SPA_ERR_INVALID_ARG;
+  TokSelArgs a{};
+  a.q_indptr = q_indptr;
+  a.mass = mass;
+  a.keep = keep;
+  a.kept = kept;
+  a.keep_count = keep_count;
+  a.token_mass = token_mass;
+  a.tau = tau;
+  a.recent = recent;
+  a.cols = mass_cols;
+  a.B = dims->num_requests;
+  a.total_q = dims->total_q;
+  a.max_q_len = dims->max_q_len;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return hip_status(timed_launch("select_tokens", s, [&] { return launch_select_tokens(a, s); }));
+}
+
 spa_status_t seg_paged_attn_validate(const spa_dims_t* dims, const int32_t* ctx_lens,
                                      const int32_t* q_indptr, const int32_t* seg_table,
                                      const int32_t* page_table, const int32_t* sel_indptr,

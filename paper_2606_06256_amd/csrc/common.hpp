@@ -96,4 +96,50 @@ __device__ __forceinline__ int lane_prefix_count(uint64_t ballot) {
   return __popcll(ballot & below);
 }
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// HBM -> LDS copy of 16 bytes per lane: bytes [voff, voff + 16) of the buffer
+// at `base` (range `bytes`; zero-range reads nothing) land at LDS byte
+// lds + 16 * lane. Inline assembly, so that the compiler does not wait for the
+// copy before each LDS read (it cannot tell the stages apart); the pipeline's
+// own waits order it. `base` and `lds` are wave-uniform.
+__device__ __forceinline__ void copy_to_lds(const void* base, int bytes, const void* lds, int voff) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  const v4i rs = {(int)__builtin_amdgcn_readfirstlane((uint32_t)b),
+                  (int)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu),
+                  __builtin_amdgcn_readfirstlane(bytes), 0x00020000};
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(m0v), "v"(voff), "s"(rs) : "m0");
+}
+
+// Block-wide exclusive prefix sum of one value per thread, in thread order,
+// and the block total (shuffle scan in each wave, then the wave totals in
+// wave order: a fixed order of additions). `scratch` holds BS / 64 values.
+template <int BS, typename T>
+__device__ void block_scan(T x, T& ex, T& tot, T* scratch) {
+  const int w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  T incl = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const T y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) scratch[w] = incl;
+  __syncthreads();
+  const T below = __shfl_up(incl, 1);     // in-wave exclusive sum (no subtraction)
+  T pre = 0;
+  tot = 0;
+#pragma unroll
+  for (int i = 0; i < BS / 64; ++i) {
+    const T c = scratch[i];
+    if (i < w) pre += c;
+    tot += c;
+  }
+  ex = lane == 0 ? pre : pre + below;
+  __syncthreads();
+}
+
 }  // namespace segpa

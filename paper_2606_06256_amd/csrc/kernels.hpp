@@ -103,6 +103,36 @@ struct ValidateArgs {
   int32_t B, Hkv, P, pps, max_segs, max_q_len, total_q, units;
 };
 
+// Attention mass of the chunk tokens (probability pass).
+struct MassArgs {
+  const __bf16* q;            // [total_q, Hq, D]
+  const int32_t* q_indptr;    // [B+1]
+  const int32_t* ctx_lens;    // [B]
+  const __bf16* k_pool;       // [n_phys, P*D], tile layout
+  const int32_t* seg_table;
+  const int32_t* page_table;
+  const int32_t* sel_indptr;
+  const int32_t* sel_pages;
+  const float* lse;           // [total_q, Hq], natural log
+  float* mass;                // [total_q, Hkv]
+  int64_t n_virtual, n_phys, sel_capacity;
+  int32_t B, Hq, Hkv, G, D, P, pps, max_segs, max_q_len, total_q;
+  int32_t key_groups;         // blocks per unit: ceil(max_q_len / keys per block)
+  float scale_log2;           // softmax scale * log2(e)
+};
+
+// Token selection by cumulative mass.
+struct TokSelArgs {
+  const int32_t* q_indptr;    // [B+1]
+  const float* mass;          // [total_q, cols]
+  uint8_t* keep;              // [total_q]
+  int32_t* kept;              // [total_q] or null
+  int32_t* keep_count;        // [B]
+  float* token_mass;          // [total_q] or null
+  double tau;
+  int32_t recent, cols, B, total_q, max_q_len;
+};
+
 constexpr int kDecodeBlock = 256;   // 4 waves
 constexpr int kSelectBlock = 512;
 constexpr int kSelectKeyCache = 4096;  // keys held in LDS by the select kernel
@@ -120,6 +150,11 @@ constexpr int kPrefillMinRows = 128;   // n_q * G at or above this runs the pref
 
 hipError_t launch_select_scores(const SelArgs& a, hipStream_t stream);
 hipError_t launch_select_fill(const SelArgs& a, hipStream_t stream);
+
+constexpr int kTokSelMax = 16384;     // longest chunk the token selection sorts in LDS
+hipError_t launch_token_mass(const MassArgs& a, hipStream_t stream);
+int token_mass_keys_per_block();
+hipError_t launch_select_tokens(const TokSelArgs& a, hipStream_t stream);
 
 hipError_t launch_page_summary(const SummaryArgs& a, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);

@@ -55,24 +55,6 @@ __device__ __forceinline__ float swap_halves(float x) {
   return __uint_as_float(__lane_id() < 32 ? r[1] : r[0]);
 }
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-// HBM -> LDS copy of 16 bytes per lane: bytes [voff, voff + 16) of the buffer
-// at `base` (range `bytes`; zero-range reads nothing) land at LDS byte
-// lds + 16 * lane. Inline assembly, so that the compiler does not wait for the
-// copy before each LDS read (it cannot tell the stages apart); the pipeline's
-// own waits order it. `base` and `lds` are wave-uniform.
-__device__ __forceinline__ void copy_to_lds(const void* base, int bytes, const void* lds, int voff) {
-  const uint64_t b = (uint64_t)(uintptr_t)base;
-  const v4i rs = {(int)__builtin_amdgcn_readfirstlane((uint32_t)b),
-                  (int)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu),
-                  __builtin_amdgcn_readfirstlane(bytes), 0x00020000};
-  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds);
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :: "s"(m0v), "v"(voff), "s"(rs) : "m0");
-}
-
 // Barrier of the key-step pipeline: this wave's LDS accesses are complete and
 // so are its copies into LDS up to two steps ahead, while the copies of later
 // steps (two per step, N in all) stay in flight. (__syncthreads would wait for

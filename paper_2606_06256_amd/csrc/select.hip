@@ -93,32 +93,6 @@ __device__ int64_t block_sum64(int64_t v, int64_t* scratch) {
   return t;
 }
 
-// Block-wide exclusive prefix sum of one int per thread, in thread order, and
-// the block total.
-template <int BS>
-__device__ void block_scan_int(int x, int& ex, int& tot, int* scratch) {
-  const int w = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
-  int incl = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(incl, o);
-    if (lane >= o) incl += y;
-  }
-  if (lane == 63) scratch[w] = incl;
-  __syncthreads();
-  int pre = 0;
-  tot = 0;
-#pragma unroll
-  for (int i = 0; i < BS / 64; ++i) {
-    const int c = scratch[i];
-    if (i < w) pre += c;
-    tot += c;
-  }
-  ex = pre + incl - x;
-  __syncthreads();
-}
-
 }  // namespace
 
 __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs a) {
@@ -209,7 +183,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
         if (tid * per < nb)
           for (int q = 0; q < per; ++q) c += (int)s_hist[tid * per + q];
         int ex, tot;
-        block_scan_int<BS>(c, ex, tot, s_scan);
+        block_scan<BS>(c, ex, tot, s_scan);
         if (c > 0 && ex < need && need <= ex + c) {
           int rem = need - ex, d = tid * per;
           for (int q = 0; q < per; ++q) {
@@ -253,7 +227,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
         const int i = c0 + tid;
         const bool m = i < nn && key_at(i) == prefix;
         int ex, tot;
-        block_scan_int<BS>(m ? 1 : 0, ex, tot, s_scan);
+        block_scan<BS>(m ? 1 : 0, ex, tot, s_scan);
         if (m && base + ex == need - 1) s_tidx = lo + i;
         base += tot;
         if (base >= need) break;
@@ -296,7 +270,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
       }
     }
     int ex, tot;
-    block_scan_int<BS>(sel ? 1 : 0, ex, tot, s_scan);
+    block_scan<BS>(sel ? 1 : 0, ex, tot, s_scan);
     if (sel) out[out_base + ex] = p;
     out_base += tot;
   }

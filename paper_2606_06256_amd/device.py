@@ -71,6 +71,26 @@ class DeviceWorkload:
                              self.sel_pages if sel_pages is None else sel_pages,
                              self.out, self.lse, self.workspace, stream)
 
+    def token_mass(self, stream=None):
+        """Mass of every chunk token per KV head, from the last fwd's lse."""
+        if getattr(self, "mass", None) is None:
+            self.mass = torch.zeros(max(1, self.wl.total_q), self.wl.Hkv, dtype=torch.float32,
+                                    device=self.device)
+        B.seg_paged_attn_token_mass(self.dims, self.q, self.q_indptr, self.ctx_lens, self.k_pool,
+                                    self.seg_table, self.page_table, self.sel_indptr,
+                                    self.sel_pages, self.lse, self.mass, stream)
+
+    def select_tokens(self, tau: float, recent: int, stream=None):
+        """Tokens kept by cumulative mass (needs token_mass() first)."""
+        if getattr(self, "keep", None) is None:
+            n = max(1, self.wl.total_q)
+            self.keep = torch.zeros(n, dtype=torch.uint8, device=self.device)
+            self.kept = torch.zeros(n, dtype=torch.int32, device=self.device)
+            self.keep_count = torch.zeros(self.wl.B, dtype=torch.int32, device=self.device)
+            self.tok_mass = torch.zeros(n, dtype=torch.float32, device=self.device)
+        B.seg_paged_attn_select_tokens(self.dims, self.q_indptr, self.mass, tau, recent, self.keep,
+                                       self.keep_count, self.kept, self.tok_mass, stream)
+
     def step(self, stream=None):
         self.select(stream)
         self.fwd(stream)

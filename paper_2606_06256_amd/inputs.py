@@ -33,6 +33,7 @@ _M32 = 0xFFFFFFFF
 
 # stream kinds; each gets its own key space
 KIND_Q, KIND_K, KIND_V, KIND_KSCALE, KIND_SHIFT_PAGE, KIND_SHIFT_DIR, KIND_PERM = 1, 2, 3, 4, 5, 6, 7
+KIND_MASS = 8
 
 
 def _lowbias32_int(x: int) -> int:
@@ -450,3 +451,28 @@ def scaled_spec(i: int, ctx_div: int = 1, batch: Optional[int] = None) -> Spec:
     return replace(sp, name=sp.name + f"_div{ctx_div}", B=B, ctx_lens=ctx, q_lens=ql,
                    seg_tokens=seg, budgets=budgets, forced_head=fh, forced_tail=ft,
                    shift_pages=cdiv(sp.shift_pages, ctx_div) if sp.shift_pages else 0)
+
+
+# --------------------------------------------------------------------------
+# synthetic per-token attention masses (inputs of the token selection)
+# --------------------------------------------------------------------------
+def synthetic_masses(seed: int, rows: int, cols: int, kind: str = "lognormal") -> np.ndarray:
+    """float32 [rows, cols] of nonnegative per-(token, head) masses.
+
+    lognormal: exp(2.5 * N(0,1)) / cols, a heavy tail like the attention mass
+      of long chunks, where a small fraction of tokens carries most of it;
+    dyadic: multiples of 2^-10 below 1/16 (many equal values; every float64
+      partial sum is exact);
+    sparse: 0 for about 90% of the entries, lognormal for the rest.
+    """
+    key = stream_key(seed, KIND_MASS, cols, {"lognormal": 0, "dyadic": 1, "sparse": 2}[kind])
+    n = rows * cols
+    if kind == "dyadic":
+        h = hash_bits(key, torch.arange(n, dtype=torch.int64)).numpy()
+        return ((h % 64).astype(np.float64) * 2.0 ** -10).astype(np.float32).reshape(rows, cols)
+    z = normals_np(key, n)
+    m = np.exp(2.5 * z) / cols
+    if kind == "sparse":
+        h = hash_bits(stream_key(seed, KIND_MASS, cols, 3), torch.arange(n, dtype=torch.int64)).numpy()
+        m = np.where(h % 10 == 0, m, 0.0)
+    return m.astype(np.float32).reshape(rows, cols)

@@ -141,3 +141,41 @@ def test_bad_append_args_rejected():
     # nothing to append: no launch, no pointer needed
     assert L.seg_paged_attn_append(ctypes.byref(d), None, None, None, None, 0, None, None, None, None,
                                    None, None) == 0
+
+
+def test_bad_token_mass_args_rejected():
+    d = _dims()
+    L = B.lib()
+    f = lambda **kw: L.seg_paged_attn_token_mass(
+        ctypes.byref(kw.get("d", d)), kw.get("q", FAKE), FAKE, FAKE, kw.get("kp", FAKE), FAKE, FAKE,
+        FAKE, FAKE, kw.get("cap", 1 << 10), kw.get("lse", FAKE), kw.get("mass", FAKE), None)
+    assert f(q=None) == -1
+    assert f(lse=None) == -1
+    assert f(mass=None) == -1
+    assert f(cap=-1) == -1
+    assert f(q=ctypes.c_void_p(0x1008)) == -1
+    assert f(kp=ctypes.c_void_p(0x1008)) == -1
+    assert f(mass=ctypes.c_void_p(0x1002)) == -1
+    assert f(d=_dims(head_dim=96)) == -2
+    # no rows: nothing launched
+    assert f(d=_dims(total_q=0)) == 0
+
+
+def test_bad_select_tokens_args_rejected():
+    d = _dims()
+    L = B.lib()
+    f = lambda **kw: L.seg_paged_attn_select_tokens(
+        ctypes.byref(kw.get("d", d)), kw.get("ind", FAKE), kw.get("mass", FAKE), kw.get("cols", 2),
+        kw.get("tau", 0.5), kw.get("recent", 0), kw.get("keep", FAKE), None, kw.get("cnt", FAKE),
+        kw.get("tm", None), None)
+    assert f(ind=None) == -1
+    assert f(mass=None) == -1
+    assert f(keep=None) == -1
+    assert f(cnt=None) == -1
+    for tau in (0.0, -0.5, 1.5, float("nan"), float("inf")):
+        assert f(tau=tau) == -1
+    assert f(recent=-1) == -1
+    assert f(cols=0) == -1
+    assert f(cols=4097) == -1
+    assert f(tm=ctypes.c_void_p(0x1002)) == -1
+    assert f(d=_dims(max_q_len=16385)) == -2
