@@ -45,7 +45,9 @@ CSRC = os.path.join(ROOT, "paper_2606_06256_amd", "csrc")
 KERNELS = {  # bench name -> (kernel symbol fragment, sources that build it)
     "decode_attn": ("decode_attn_kernel", ["common.hpp", "kernels.hpp", "decode.hip"]),
     "prefill_attn": ("prefill_kernel", ["common.hpp", "kernels.hpp", "prefill.hip"]),
+    "token_mass": ("token_mass_kernel", ["common.hpp", "kernels.hpp", "mass.hip"]),
 }
+OP_OF_KERNEL = {"token_mass": "--op token_mass "}   # bench arguments that run the kernel
 COPY_KERNEL = "copyBuffer"
 
 
@@ -100,7 +102,7 @@ def pmc_command(bench_args):
     """The counter runs behind an entry: one pass per counter, from /tmp on
     the GPU host, with the repository root in $R."""
     return ("cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc {FETCH_SIZE|WRITE_SIZE} "
-            "--kernel-include-regex 'decode_attn|prefill_kernel|copyBuffer' --output-format csv "
+            "--kernel-include-regex 'decode_attn|prefill_kernel|token_mass|copyBuffer' --output-format csv "
             f"-d <out_dir> -o run -- python3 $R/bench.py {bench_args}")
 
 
@@ -134,7 +136,8 @@ def write_traffic_entry(args):
         "hbm_read_bytes": int(read_b), "hbm_write_bytes": int(write_b),
         "hbm_bytes_per_launch": int(read_b + write_b),
         "sources_sha256": kernel_sources_sha256(args.kernel),
-        "command": pmc_command(f"--steps 5 --warmup 2 --no-cpu-baseline --workload {args.workload}"),
+        "command": pmc_command(OP_OF_KERNEL.get(args.kernel, "")
+                               + f"--steps 5 --warmup 2 --no-cpu-baseline --workload {args.workload}"),
     }
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as f:
@@ -422,8 +425,8 @@ def bench_token_mass(args, wl, tau=0.2, recent=128):
                    "token_mass_mfma_frac": round(tfs / MFMA_BF16_PEAK_TFLOPS, 4)},
         "roofline": {"kernel": "token_mass", "bound": "hbm", "achieved": round(gbs, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_launch": abytes, "flops_per_launch": flops,
-                     "launch_ms": round(mass_ms, 5)},
+                     "traffic": recorded_traffic("token_mass", wl.spec.name), "bytes_per_launch": abytes,
+                     "flops_per_launch": flops, "launch_ms": round(mass_ms, 5)},
     }), flush=True)
 
 
