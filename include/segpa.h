@@ -239,8 +239,8 @@ spa_status_t seg_paged_attn_rope_align(const spa_dims_t* dims, void* k_pool, con
                                        void* stream);
 
 /*
- * Page key summary for TOPK_MEANKEY (this build's content rule; the paper
- * states none): page_ksum[p][d] = float32 rounding of the sum over the first
+ * Page key summary for TOPK_MEANKEY (a content rule of this library; the
+ * paper states none): page_ksum[p][d] = float32 rounding of the sum over the first
  * page_valid_tokens[p] tokens of physical page p of K[token][d], accumulated in
  * float64 (exact when the page's nonzero magnitudes span less than 2^40).
  * In:  k_pool device bf16 [num_phys_pages, P * D]; page_valid_tokens device

@@ -26,7 +26,7 @@ Readings where the paper is silent (each listed in the design notes):
   queries sits at the end of the context (query i at position L - n_q + i) and
   is causal; the sink set is the first n_sink token positions; an empty key set
   gives O = 0 and LSE = -inf; budgets are whole pages per request; RANDOM_HASH
-  and TOPK_MEANKEY are the two content/seeded rules of this build (the paper's
+  and TOPK_MEANKEY are content/seeded rules defined here, not in the paper (its
   only KV page rule is the head-class policy, HEAD_CLASS here).
 
 All floating point is float64; bf16 inputs convert exactly.

@@ -124,13 +124,13 @@ def test_token_mass_scaled_prefill_workloads(i, div, batch):
     _require_gpu()
     sp = I.scaled_spec(i, div, batch)
     wl = I.build(sp)
-    dw = _gpu_masses(wl, f"cfg{i}/div{div}")
+    dw = _gpu_masses(wl, sp.name)
     q64 = wl.q("cpu").double().numpy()
     units = PU.sample_units(wl.num_units, 3)
     sel = PU.oracle_selection(wl, q64, units=units)
     PU.compare_selection(wl, dw, q64, sel)
     worst = _check_unit_masses(wl, dw, q64, sel, units)
-    print(f"[mass] cfg{i}: worst relative error {worst:.3e}", flush=True)
+    print(f"[mass] {sp.name}: worst relative error {worst:.3e}", flush=True)
 
 
 def test_token_mass_is_reproducible():
@@ -308,7 +308,7 @@ def _selection_properties(tm, keep, kept, cnt, q0, n, tau, recent):
 def test_full_size_headclass_prefill_sampled():
     _require_gpu()
     wl = I.config(9)
-    dw = _gpu_masses(wl, "cfg9/full")
+    dw = _gpu_masses(wl, wl.spec.name + "/full")
     tau, recent = 0.2, 128
     dw.select_tokens(tau, recent)
     torch.cuda.synchronize()

@@ -41,7 +41,7 @@ def test_tiny_config_full():
 @pytest.mark.parametrize("i,div,batch", [(2, 16, 4), (3, 32, 6), (5, 32, 3)])
 def test_scaled_decode_configs(i, div, batch):
     _require_gpu()
-    PU.run_parity(I.build(I.scaled_spec(i, div, batch)), label=f"cfg{i}/div{div}")
+    PU.run_parity(I.build(I.scaled_spec(i, div, batch)))
 
 
 @pytest.mark.parametrize("i,div,batch", [(6, 1, 4), (7, 8, 3), (8, 32, 2), (9, 16, 3)])
@@ -49,7 +49,7 @@ def test_scaled_headclass_configs(i, div, batch):
     """The head-class micro-benchmark shape (global and local KV heads, one
     batched call over layers), decode and chunked prefill, at reduced sizes."""
     _require_gpu()
-    PU.run_parity(I.build(I.scaled_spec(i, div, batch)), label=f"cfg{i}/div{div}")
+    PU.run_parity(I.build(I.scaled_spec(i, div, batch)))
 
 
 def test_scaled_prefill_config():
@@ -59,7 +59,7 @@ def test_scaled_prefill_config():
     sp.ctx_lens = [2048 + 48, 1500 + 31]
     sp.budgets = [40, 30]
     sp.forced_tail = 3
-    PU.run_parity(I.build(sp), label="cfg4/small")
+    PU.run_parity(I.build(sp), label="chunked_prefill/small")
 
 
 # --------------------------------------------------------------------------
@@ -286,4 +286,4 @@ def test_full_size_config(i):
     units = PU.sample_units(U, 3)
     # selections: every unit for the seeded rules, sampled units for TOPK
     sel_units = units if wl.spec.sel_mode == I.SEL_TOPK_MEANKEY else None
-    PU.run_parity(wl, units=units, sel_units=sel_units, label=f"cfg{i}/full")
+    PU.run_parity(wl, units=units, sel_units=sel_units, label=wl.spec.name + "/full")
