@@ -85,6 +85,10 @@ def _check_unit_masses(wl, dw, q64, sel, units):
 
 MASS_CASES = {
     "two_key_groups_ragged": dict(q_lens=[300, 77], ctx_lens=[900, 77]),
+    # chunks longer than one block's 512 keys: several key groups per unit
+    "key_groups_2_and_3": dict(Hq=4, Hkv=2, q_lens=[700, 1100], ctx_lens=[1500, 1100],
+                               seg_tokens=512),
+    "key_groups_d64_g8": dict(D=64, Hq=16, Hkv=2, q_lens=[530, 513], ctx_lens=[600, 800]),
     "chunk_is_whole_stream": dict(q_lens=[64, 16], ctx_lens=[64, 16]),
     "decode_rows": dict(q_lens=[1, 1], ctx_lens=[700, 5]),
     "short_chunks": dict(q_lens=[3, 7], ctx_lens=[300, 129]),
