@@ -104,6 +104,14 @@ EDGE = {
                                q_lens=[40, 40], ctx_lens=[900, 300]),
     "prefill_rows_g16": dict(Hq=32, Hkv=2, q_lens=[33, 17], ctx_lens=[600, 256]),
     "prefill_many_entries": dict(ctx_lens=[20000, 3000], q_lens=[40, 8], seg_tokens=4096),
+    # the largest page sizes: several 16-token tiles per page, partial last pages
+    "page128": dict(P=128, seg_tokens=512, ctx_lens=[1000, 130]),
+    "page256_d64": dict(P=256, seg_tokens=1024, D=64, ctx_lens=[2000, 257], q_lens=[3, 1]),
+    "page128_prefill": dict(P=128, seg_tokens=512, ctx_lens=[900, 400], q_lens=[70, 40]),
+    "page256_random": dict(P=256, seg_tokens=1024, sel_mode=I.SEL_RANDOM_HASH, budgets=[3, 2],
+                           forced_tail=1, ctx_lens=[3000, 1500], q_lens=[1, 1], sel_seed=9),
+    "page128_topk": dict(P=128, seg_tokens=512, sel_mode=I.SEL_TOPK_MEANKEY, budgets=[4, 2],
+                         ctx_lens=[1800, 700]),
 }
 
 
@@ -111,6 +119,42 @@ EDGE = {
 def test_edge_cases(name):
     _require_gpu()
     PU.run_parity(I.build(_spec(name=name, **EDGE[name])), label=name)
+
+
+def _random_spec(k: int):
+    """A seeded random small workload: shapes, page sizes, chunk lengths,
+    selection rules and their parameters all drawn from the supported ranges."""
+    rng = np.random.default_rng(900 + k)
+    Hkv = int(rng.choice([1, 2, 4]))
+    G = int(rng.choice([1, 2, 3, 4, 8, 16]))
+    D = int(rng.choice([64, 128]))
+    P = int(rng.choice([16, 32, 64, 128, 256]))
+    seg = P * int(rng.choice([1, 2, 4, 8]))
+    B = int(rng.integers(1, 4))
+    ctx = rng.integers(1, 1500, size=B)
+    ql = [int(min(c, rng.choice([1, 1, 2, 5, 17, 40, 64]))) for c in ctx]
+    mode = int(rng.choice([I.SEL_ALL, I.SEL_HEAD_CLASS, I.SEL_RANDOM_HASH, I.SEL_TOPK_MEANKEY]))
+    npg = [-(-int(c) // P) for c in ctx]
+    kw = dict(name=f"random{k}", B=B, Hq=Hkv * G, Hkv=Hkv, D=D, P=P, seg_tokens=seg,
+              ctx_lens=ctx.tolist(), q_lens=ql, seed=5000 + k, sel_mode=mode)
+    if mode in (I.SEL_RANDOM_HASH, I.SEL_TOPK_MEANKEY):
+        kw["budgets"] = [int(rng.integers(0, n + 2)) for n in npg]
+        kw["forced_head"] = int(rng.integers(0, 3))
+        kw["forced_tail"] = int(rng.integers(0, 3))
+        kw["sel_seed"] = int(rng.integers(0, 1 << 62))
+    if mode == I.SEL_HEAD_CLASS:
+        kw["head_policy"] = rng.integers(0, 2, size=Hkv).tolist()
+        kw["n_sink"] = int(rng.integers(0, 40))
+        kw["window"] = int(rng.integers(0, 600))
+    return I.Spec(**kw)
+
+
+@pytest.mark.parametrize("k", range(16))
+def test_random_small_workloads(k):
+    _require_gpu()
+    sp = _random_spec(k)
+    PU.run_parity(I.build(sp), label=f"{sp.name} B={sp.B} G={sp.Hq // sp.Hkv} D={sp.D} P={sp.P} "
+                  f"q={list(sp.q_lens)} mode={sp.sel_mode}")
 
 
 def test_many_units_short_lists():
