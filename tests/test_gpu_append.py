@@ -28,6 +28,8 @@ CASES = {
     "some_requests_idle": dict(D=128, P=64, seg=128, L1=[500, 260, 90], n=[0, 130, 0]),
     "past_the_table": dict(D=128, P=16, seg=64, L1=[100, 40], n=[20, 5], extra=[9, 0]),
     "unmapped_segment": dict(D=128, P=16, seg=32, L1=[200, 150], n=[60, 10], unmap=(0, 1, 5)),
+    "page128": dict(D=128, P=128, seg=256, L1=[250, 129, 600], n=[10, 129, 300]),
+    "page256_d64": dict(D=64, P=256, seg=512, L1=[600, 200], n=[300, 56]),
 }
 
 

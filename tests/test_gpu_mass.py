@@ -97,6 +97,10 @@ MASS_CASES = {
     "g3": dict(Hq=6, Hkv=2, q_lens=[50, 20], ctx_lens=[500, 90]),
     "g16": dict(Hq=32, Hkv=2, q_lens=[33, 17], ctx_lens=[600, 256]),
     "page64": dict(P=64, seg_tokens=512, q_lens=[100, 70], ctx_lens=[700, 400]),
+    "page256_key_groups": dict(P=256, seg_tokens=512, D=64, q_lens=[600, 90],
+                               ctx_lens=[1300, 300]),
+    "page128_random_gaps": dict(P=128, seg_tokens=256, sel_mode=I.SEL_RANDOM_HASH, budgets=[4, 2],
+                                q_lens=[300, 60], ctx_lens=[1500, 400], sel_seed=41),
     # a small page budget without the forced tail leaves chunk pages unselected
     "random_chunk_gaps": dict(sel_mode=I.SEL_RANDOM_HASH, budgets=[10, 6], q_lens=[64, 40],
                               ctx_lens=[600, 300], sel_seed=31),
