@@ -102,7 +102,11 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 // at `base` (range `bytes`; zero-range reads nothing) land at LDS byte
 // lds + 16 * lane. Inline assembly, so that the compiler does not wait for the
 // copy before each LDS read (it cannot tell the stages apart); the pipeline's
-// own waits order it. `base` and `lds` are wave-uniform.
+// own waits order it. `base` and `lds` are wave-uniform. The compiler's hazard
+// checks do not see into the assembly, so it keeps the wait states GFX9 asks
+// for itself: 5 between a vector instruction writing an SGPR (the descriptor
+// comes out of v_readfirstlane) and a memory instruction reading it, and 1
+// between the M0 write and the LDS-destination load (s_mov + s_nop 4 = 6).
 __device__ __forceinline__ void copy_to_lds(const void* base, int bytes, const void* lds, int voff) {
   const uint64_t b = (uint64_t)(uintptr_t)base;
   const v4i rs = {(int)__builtin_amdgcn_readfirstlane((uint32_t)b),
@@ -110,7 +114,7 @@ __device__ __forceinline__ void copy_to_lds(const void* base, int bytes, const v
                   __builtin_amdgcn_readfirstlane(bytes), 0x00020000};
   const uint32_t m0v = __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds);
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :: "s"(m0v), "v"(voff), "s"(rs) : "m0");
 }
 
