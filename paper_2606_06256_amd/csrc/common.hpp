@@ -99,23 +99,33 @@ __device__ __forceinline__ int lane_prefix_count(uint64_t ballot) {
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 // HBM -> LDS copy of 16 bytes per lane: bytes [voff, voff + 16) of the buffer
-// at `base` (range `bytes`; zero-range reads nothing) land at LDS byte
-// lds + 16 * lane. Inline assembly, so that the compiler does not wait for the
-// copy before each LDS read (it cannot tell the stages apart); the pipeline's
-// own waits order it. `base` and `lds` are wave-uniform. The compiler's hazard
-// checks do not see into the assembly, so it keeps the wait states GFX9 asks
-// for itself: 5 between a vector instruction writing an SGPR (the descriptor
-// comes out of v_readfirstlane) and a memory instruction reading it, and 1
-// between the M0 write and the LDS-destination load (s_mov + s_nop 4 = 6).
-__device__ __forceinline__ void copy_to_lds(const void* base, int bytes, const void* lds, int voff) {
+// at `base` (range `bytes`; zero-range reads nothing) land at LDS byte address
+// lds_byte + 16 * lane. Inline assembly, so that the compiler does not wait
+// for the copy before each LDS read (it cannot tell the stages apart); the
+// pipeline's own waits order it. `base` and `lds_byte` are wave-uniform (a
+// caller that computes the address with scalar arithmetic keeps the chain off
+// the vector unit). The compiler's hazard checks do not see into the
+// assembly, so it keeps the wait states GFX9 asks for itself: 5 between a
+// vector instruction writing an SGPR (the descriptor comes out of
+// v_readfirstlane) and a memory instruction reading it, and 1 between the M0
+// write and the LDS-destination load (s_mov + s_nop 4 = 6).
+__device__ __forceinline__ void copy_to_lds_at(const void* base, int bytes, uint32_t lds_byte, int voff) {
   const uint64_t b = (uint64_t)(uintptr_t)base;
   const v4i rs = {(int)__builtin_amdgcn_readfirstlane((uint32_t)b),
                   (int)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu),
                   __builtin_amdgcn_readfirstlane(bytes), 0x00020000};
-  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds);
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_byte);
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :: "s"(m0v), "v"(voff), "s"(rs) : "m0");
+}
+
+// LDS byte address of a pointer into LDS
+__device__ __forceinline__ uint32_t lds_address(const void* lds) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds;
+}
+
+__device__ __forceinline__ void copy_to_lds(const void* base, int bytes, const void* lds, int voff) {
+  copy_to_lds_at(base, bytes, lds_address(lds), voff);
 }
 
 // Block-wide exclusive prefix sum of one value per thread, in thread order,

@@ -159,6 +159,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
   for (int i = tid * 16; i < (int)sizeof(s_kv); i += kPfThreads * 16)
     *reinterpret_cast<s16x8*>(s_kv + i) = (s16x8){0, 0, 0, 0, 0, 0, 0, 0};
 
+  const uint32_t kv_lds = __builtin_amdgcn_readfirstlane(lds_address(s_kv));
   bool done = false;
   for (int ce = 0; ce < n_e && !done; ce += kPfEntries) {
     const int cn = min(kPfEntries, n_e - ce);
@@ -225,14 +226,17 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
 
     // HBM -> LDS copy of this wave's share of step x; unusable tiles use a
     // zero-range descriptor (no bytes are read)
+    // (the addresses are scalar arithmetic on the table entry and this wave's
+    // LDS slot offset, with no vector-register round trip)
+    const uint32_t my_lds = __builtin_amdgcn_readfirstlane((uint32_t)(ct * TB + part * 1024));
     auto issue_copy = [&](int x) {
       if (!mover) return;
-      const int tile = (int)((uint32_t)__builtin_amdgcn_readlane(tab, x - tb) >> 3) - 1;
-      const int64_t base = uniform64((int64_t)(tile < 0 ? 0 : tile) * (kTile * D));
-      const int range = tile >= 0 ? TB : 0;
-      const char* sg = stage(x);
-      copy_to_lds(a.k_pool + base, range, sg + ct * TB + part * 1024, k_off);
-      copy_to_lds(a.v_pool + base, range, sg + 2 * TB + ct * TB + part * 1024, v_off);
+      const uint32_t ent = (uint32_t)__builtin_amdgcn_readlane(tab, x - tb);
+      const int64_t tile = ent >= 8 ? (int64_t)(ent >> 3) - 1 : 0;
+      const int range = ent >= 8 ? TB : 0;
+      const uint32_t dst = kv_lds + (uint32_t)((x & (kPfStages - 1)) * SB) + my_lds;
+      copy_to_lds_at(a.k_pool + tile * (kTile * D), range, dst, k_off);
+      copy_to_lds_at(a.v_pool + tile * (kTile * D), range, dst + 2 * TB, v_off);
     };
     // A tile that ends past the context: its V slots there are rewritten as
     // zeros (their probability is 0, and stale contents there must not reach
