@@ -177,8 +177,9 @@ spa_status_t seg_paged_attn_select(const spa_dims_t* dims, const spa_select_para
  *      [num_virtual_pages]; sel_indptr device [B*Hkv+1]; sel_pages device
  *      [sel_capacity] (entries past sel_capacity are never read).
  * Out: out device bf16 [total_q, Hq, D]; lse device fp32 [total_q, Hq] or NULL.
- * Shapes: max_q_len * G <= 16 runs the decode kernel (one matrix-core tile of
- * query rows per unit); larger chunks run the chunked-prefill kernel.
+ * Shapes: max_q_len * G < 128 runs the split-KV decode kernel (the query rows
+ * of a unit in blocks of 16, one matrix-core tile each); larger chunks run the
+ * chunked-prefill kernel.
  */
 spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int32_t* q_indptr,
                                 const int32_t* ctx_lens, const void* k_pool, const void* v_pool,
