@@ -275,15 +275,18 @@ __global__ __launch_bounds__(kDecodeBlock) void decode_attn_kernel(const FwdArgs
 }
 
 // Merge the split partials of every virtual unit (unit, row block) that spans
-// several waves; write O = 0, LSE = -inf for units without selected tiles.
-// One block per virtual unit. All partial loads of a phase are independent
-// (no load waits for the previous one): the per-row max and sum come from a
-// block reduction, then every output element sums its partials.
+// several waves (log-sum-exp, Section 4.4); write O = 0, LSE = -inf for units
+// without selected tiles. One block per virtual unit, 16 threads per query row,
+// each with D / 16 output dims. A thread issues the row LSEs and its dims of 8
+// partials at once (no load waits for another), so a batch of 8 partials
+// costs one memory round trip; batches are merged in wave order with one
+// rescale each, so the result does not depend on timing.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(const FwdArgs a) {
   constexpr int kRows = 16;
-  constexpr int kLanesPerRow = 256 / kRows;     // 16 threads per row in the reductions
-  constexpr int kCacheW = 64;                   // partial LSEs kept in LDS
+  constexpr int TPR = 256 / kRows;     // threads per row
+  constexpr int NQ = D / TPR / 4;      // float4 groups per thread
+  constexpr int WB = 8;                // partials per batch
   const int RB = a.row_blocks;
   const int v = blockIdx.x;
   const int u = v / RB;
@@ -301,9 +304,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const FwdArgs a) {
   const int G = a.G;
   const int q0 = clampv(a.q_indptr[r], 0, a.total_q);
   const int nq = clampv(a.q_indptr[r + 1] - q0, 0, min(a.max_q_len, a.total_q - q0));
-  const int row0 = rb * kRows;
-  const int rows = min(kRows, nq * G - row0);
-  if (rows <= 0) return;
+  const int row = threadIdx.x / TPR;
+  const int d0 = (threadIdx.x % TPR) * (4 * NQ);
+  const int R = rb * kRows + row;
+  if (R >= nq * G) return;
 
   // must mirror the decode kernel's partition
   const bool empty = nt <= 0;
@@ -315,71 +319,47 @@ __global__ __launch_bounds__(256) void combine_kernel(const FwdArgs a) {
     if (nw == 1) return;   // one wave wrote the final output
   }
   const int64_t sbase = (int64_t)u * RB + rb + w0;   // slot of the first partial
-  __shared__ float s_lse[kCacheW][kRows];
-  __shared__ float s_red[kRows][kLanesPerRow];
-  __shared__ float s_m[kRows], s_z[kRows];
-  const int tid = threadIdx.x;
-  const int row = tid % kRows;
-  const int lane_r = tid / kRows;
-
-  if (!empty) {
-    // row max over partials
-    float M = -INFINITY;
-    for (int64_t w = lane_r; w < nw; w += kLanesPerRow) {
-      const float x = a.part_lse[(sbase + w) * kRows + row];
-      if (w < kCacheW) s_lse[w][row] = x;
-      M = fmaxf(M, x);
+  float M = -INFINITY, Z = 0.f;
+  f32x4 o[NQ];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) o[i] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  for (int64_t w = 0; w < nw; w += WB) {
+    float x[WB];
+    f32x4 po[WB][NQ];
+#pragma unroll
+    for (int k = 0; k < WB; ++k) {
+      const int64_t s = sbase + min(w + k, nw - 1);
+      x[k] = w + k < nw ? a.part_lse[s * kRows + row] : -INFINITY;
+#pragma unroll
+      for (int i = 0; i < NQ; ++i)
+        po[k][i] = *reinterpret_cast<const f32x4*>(a.part_o + (s * kRows + row) * D + d0 + 4 * i);
     }
-    s_red[row][lane_r] = M;
-    __syncthreads();
-    if (tid < kRows) {
-      float mm = -INFINITY;
-      for (int i = 0; i < kLanesPerRow; ++i) mm = fmaxf(mm, s_red[tid][i]);
-      s_m[tid] = mm;
+    float mb = M;
+#pragma unroll
+    for (int k = 0; k < WB; ++k) mb = fmaxf(mb, x[k]);
+    if (mb == -INFINITY) continue;             // nothing visible so far
+    const float sc = fast_exp2(M - mb);        // 0 while M is -inf
+    Z *= sc;
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) o[i] *= sc;
+#pragma unroll
+    for (int k = 0; k < WB; ++k) {
+      const float wt = fast_exp2(x[k] - mb);  // 0 for x = -inf
+      Z += wt;
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) o[i] += wt * po[k][i];
     }
-    __syncthreads();
-    const float Mr = s_m[row];
-    float Z = 0.f;
-    if (Mr != -INFINITY)
-      for (int64_t w = lane_r; w < nw; w += kLanesPerRow) {
-        const float x = w < kCacheW ? s_lse[w][row] : a.part_lse[(sbase + w) * kRows + row];
-        Z += fast_exp2(x - Mr);
-      }
-    s_red[row][lane_r] = Z;
-    __syncthreads();
-    if (tid < kRows) {
-      float zz = 0.f;
-      for (int i = 0; i < kLanesPerRow; ++i) zz += s_red[tid][i];
-      s_z[tid] = zz;
-    }
-    __syncthreads();
+    M = mb;
   }
-  // outputs: 4 consecutive dims per thread
-  for (int idx = tid; idx < rows * (D / 4); idx += blockDim.x) {
-    const int rr = idx / (D / 4);
-    const int d = (idx - rr * (D / 4)) * 4;
-    const int R = row0 + rr;
-    const int qi = R / G;
-    const int hh = R - qi * G;
-    const int64_t orow = (int64_t)(q0 + qi) * a.Hq + g * G + hh;
-    f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    float lse = -INFINITY;
-    if (!empty && s_z[rr] > 0.f) {
-      const float M = s_m[rr];
-      const float Z = s_z[rr];
-#pragma unroll 8
-      for (int64_t w = 0; w < nw; ++w) {
-        const float x = w < kCacheW ? s_lse[w][rr] : a.part_lse[(sbase + w) * kRows + rr];
-        const float wt = fast_exp2(x - M);
-        const f32x4 po = *reinterpret_cast<const f32x4*>(a.part_o + ((sbase + w) * kRows + rr) * D + d);
-        o += wt * po;
-      }
-      o *= 1.f / Z;
-      lse = (M + __log2f(Z)) * kLn2;
-    }
-    *reinterpret_cast<s16x4*>(a.out + orow * D + d) = pack_bf16x4(o[0], o[1], o[2], o[3]);
-    if (d == 0 && a.lse != nullptr) a.lse[orow] = lse;
-  }
+  const int qi = R / G;
+  const int hh = R - qi * G;
+  const int64_t orow = (int64_t)(q0 + qi) * a.Hq + g * G + hh;
+  const float iz = Z > 0.f ? 1.f / Z : 0.f;
+#pragma unroll
+  for (int i = 0; i < NQ; ++i)
+    *reinterpret_cast<s16x4*>(a.out + orow * D + d0 + 4 * i) =
+        pack_bf16x4(o[i][0] * iz, o[i][1] * iz, o[i][2] * iz, o[i][3] * iz);
+  if (d0 == 0 && a.lse != nullptr) a.lse[orow] = Z > 0.f ? (M + __log2f(Z)) * kLn2 : -INFINITY;
 }
 
 hipError_t launch_decode(const FwdArgs& a, hipStream_t stream) {
