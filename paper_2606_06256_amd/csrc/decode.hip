@@ -106,6 +106,11 @@ __device__ void decode_unit_range(const FwdArgs& a, int u, int rb, int64_t nt, i
   }
 
   const int32_t* seg_row = a.seg_table + (int64_t)u * a.max_segs;
+  // The unit's segment-table row, one entry per lane, read alongside the
+  // first selected ids: a page's segment lookup is then a lane shuffle, one
+  // dependent memory round trip less before the first K/V tile.
+  const bool seg_in_regs = a.max_segs <= kWave;
+  const int seg_lane = seg_in_regs && lane < a.max_segs ? seg_row[lane] : -1;
   const int koff = (grp * kTile + j) * 16;   // byte offsets inside a tile
   const int voff = j * kTile * 2 + grp * 8;
   const int tpp_log2 = a.tpp_log2;
@@ -154,13 +159,22 @@ __device__ void decode_unit_range(const FwdArgs& a, int u, int rb, int64_t nt, i
   const int64_t e_first = la >> tpp_log2;
   const int64_t e_last = (lb - 1) >> tpp_log2;
   for (int64_t eb = e_first; eb <= e_last; eb += kWave) {
-    int b_jpg = -1, b_ph = -1;
-    if (eb + lane <= e_last) {
-      b_jpg = a.sel_pages[e_unit0 + eb + lane];
-      if (b_jpg >= 0 && b_jpg < npg)
-        b_ph = translate_page(seg_row, a.page_table, b_jpg, a.pps, a.max_segs, a.n_virtual, a.n_phys);
-      else
-        b_jpg = -1;
+    int b_jpg = eb + lane <= e_last ? a.sel_pages[e_unit0 + eb + lane] : -1;
+    if (!(b_jpg >= 0 && b_jpg < npg)) b_jpg = -1;
+    int b_ph = -1;
+    if (seg_in_regs) {
+      // (the shuffle runs with every lane active; jp < npg keeps s < max_segs)
+      const int sidx = b_jpg >= 0 ? b_jpg / a.pps : 0;
+      const int v0 = __shfl(seg_lane, sidx);
+      if (b_jpg >= 0 && v0 >= 0) {
+        const int64_t vp = (int64_t)v0 + (b_jpg - sidx * a.pps);
+        if (vp < a.n_virtual) {
+          const int ph = a.page_table[vp];
+          b_ph = ph >= 0 && (int64_t)ph < a.n_phys ? ph : -1;
+        }
+      }
+    } else if (b_jpg >= 0) {
+      b_ph = translate_page(seg_row, a.page_table, b_jpg, a.pps, a.max_segs, a.n_virtual, a.n_phys);
     }
     const int64_t t0 = max(la, eb << tpp_log2);
     const int64_t t1 = min(lb, (eb + kWave) << tpp_log2);
