@@ -32,19 +32,39 @@ struct UnitInfo {
   int b_begin;  // HEAD_CLASS: window pages [b_begin, n); ranked: forced tail [b_begin, n)
 };
 
-__device__ UnitInfo unit_info(const SelArgs& a, int u) {
+// The per-unit inputs of the closed-form counts, read in one go so that a
+// block can issue them early and do the arithmetic later.
+struct UnitRaw {
+  int L;        // context length (unclamped)
+  int q0, q1;   // HEAD_CLASS: query range of the request
+  int local;    // HEAD_CLASS: 1 for a local head
+  int budget;   // RANDOM_HASH / TOPK: budget of the request
+};
+
+__device__ UnitRaw load_unit(const SelArgs& a, int u) {
   const int r = u / a.Hkv;
   const int g = u - r * a.Hkv;
+  UnitRaw x{a.ctx_lens[r], 0, 1, 0, 0};
+  if (a.mode == kModeHeadClass) {
+    x.local = a.head_policy[g] == 0;
+    if (a.q_indptr != nullptr) { x.q0 = a.q_indptr[r]; x.q1 = a.q_indptr[r + 1]; }
+  } else if (a.mode == kModeRandom || a.mode == kModeTopk) {
+    x.budget = a.budget[r];
+  }
+  return x;
+}
+
+__device__ UnitInfo unit_info_of(const SelArgs& a, const UnitRaw& x) {
   const int max_tokens = a.max_segs * a.pps * a.P;
-  const int L = clampv(a.ctx_lens[r], 0, max_tokens);
+  const int L = clampv(x.L, 0, max_tokens);
   UnitInfo I;
   I.n = (L + a.P - 1) / a.P;
   I.count = I.n;
   I.a_end = I.n;
   I.b_begin = I.n;
   if (a.mode == kModeHeadClass) {
-    if (a.head_policy[g] == 0) {   // local head
-      const int nq = a.q_indptr != nullptr ? clampv(a.q_indptr[r + 1] - a.q_indptr[r], 0, L) : 1;
+    if (x.local) {
+      const int nq = clampv(x.q1 - x.q0, 0, L);
       const int ns = clampv(a.n_sink, 0, L);
       const int sinkp = min(I.n, (ns + a.P - 1) / a.P);
       const int winlo = nq > 0 ? min(I.n, max(0, L - nq - a.window) / a.P) : I.n;
@@ -57,13 +77,15 @@ __device__ UnitInfo unit_info(const SelArgs& a, int u) {
     const int fh = min(I.n, a.forced_head);
     const int ft = min(I.n, a.forced_tail);
     const int forced = min(I.n, fh + ft);
-    const int b = max(0, a.budget[r]);
+    const int b = max(0, x.budget);
     I.a_end = fh;
     I.b_begin = max(fh, I.n - ft);
     I.count = min(I.n, max(b, forced));
   }
   return I;
 }
+
+__device__ UnitInfo unit_info(const SelArgs& a, int u) { return unit_info_of(a, load_unit(a, u)); }
 
 __device__ __forceinline__ uint64_t random_key(uint64_t sm_seed, int r, int g, int p) {
   return splitmix64(sm_seed ^ (((uint64_t)r << 40) | ((uint64_t)g << 32) | (uint32_t)p));
@@ -111,18 +133,34 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
   const int r = u / a.Hkv;
   const int g = u - r * a.Hkv;
 
-  int64_t part = 0;
-  for (int v = tid; v < u; v += BS) part += unit_info(a, v).count;
-  const int64_t offset = block_sum64<BS>(part, s_red);
-  const UnitInfo I = unit_info(a, u);
-  if (tid == 0) {
-    a.sel_indptr[u + 1] = (int32_t)(offset + I.count);
-    if (u == 0) a.sel_indptr[0] = 0;
+  // CSR offset = the counts of the earlier units. The inputs of the first
+  // kPre of them per thread are loaded here and summed only before the
+  // output is written, so their latency overlaps the ranking.
+  constexpr int kPre = 2;
+  UnitRaw pre[kPre];
+#pragma unroll
+  for (int k = 0; k < kPre; ++k) {
+    const int v = tid + k * BS;
+    if (v < u) pre[k] = load_unit(a, v);
   }
-  int32_t* out = a.sel_pages + offset;
+  auto csr_offset = [&]() -> int64_t {
+    int64_t part = 0;
+#pragma unroll
+    for (int k = 0; k < kPre; ++k)
+      if (tid + k * BS < u) part += unit_info_of(a, pre[k]).count;
+    for (int v = tid + kPre * BS; v < u; v += BS) part += unit_info(a, v).count;
+    return block_sum64<BS>(part, s_red);
+  };
+  const UnitInfo I = unit_info(a, u);
   const int n = I.n;
 
   if (a.mode == kModeAll || a.mode == kModeHeadClass) {
+    const int64_t offset = csr_offset();
+    if (tid == 0) {
+      a.sel_indptr[u + 1] = (int32_t)(offset + I.count);
+      if (u == 0) a.sel_indptr[0] = 0;
+    }
+    int32_t* out = a.sel_pages + offset;
     // ascending union of [0, a_end) and [b_begin, n)
     for (int i = tid; i < I.count; i += BS)
       out[i] = i < I.a_end ? i : I.b_begin + (i - I.a_end);
@@ -255,23 +293,41 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
     pT = s_tidx;
   }
 
-  // ascending emission: forced pages and the chosen pages
+  const int64_t offset = csr_offset();
+  if (tid == 0) {
+    a.sel_indptr[u + 1] = (int32_t)(offset + I.count);
+    if (u == 0) a.sel_indptr[0] = 0;
+  }
+  int32_t* out = a.sel_pages + offset;
+
+  // ascending emission: forced pages and the chosen pages, four consecutive
+  // pages per thread (one block prefix count per 4 * BS pages)
+  constexpr int kPer = 4;
   int out_base = 0;
-  for (int c0 = 0; c0 < n; c0 += BS) {
-    const int p = c0 + tid;
-    const bool in = p < n;
-    const bool nonforced = in && p >= lo && p < hi;
-    bool sel = in && !nonforced;
-    if (nonforced) {
-      if (take_all) sel = true;
-      else if (!take_none) {
-        const uint64_t k = cached ? s_keys[p - lo] : key_of(p);
-        sel = k < T || (k == T && p <= pT);
+  for (int c0 = 0; c0 < n; c0 += kPer * BS) {
+    bool sel[kPer];
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+      const int p = c0 + tid * kPer + e;
+      const bool in = p < n;
+      const bool nonforced = in && p >= lo && p < hi;
+      sel[e] = in && !nonforced;
+      if (nonforced) {
+        if (take_all) sel[e] = true;
+        else if (!take_none) {
+          const uint64_t k = cached ? s_keys[p - lo] : key_of(p);
+          sel[e] = k < T || (k == T && p <= pT);
+        }
       }
+      cnt += sel[e] ? 1 : 0;
     }
     int ex, tot;
-    block_scan<BS>(sel ? 1 : 0, ex, tot, s_scan);
-    if (sel) out[out_base + ex] = p;
+    block_scan<BS>(cnt, ex, tot, s_scan);
+    int o = out_base + ex;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e)
+      if (sel[e]) out[o++] = c0 + tid * kPer + e;
     out_base += tot;
   }
 }
