@@ -186,8 +186,18 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
   uint64_t T = 0;
   int pT = -1;
   if (!take_all && !take_none) {
-    if (cached)
-      for (int i = tid; i < nn; i += BS) s_keys[i] = key_of(lo + i);
+    // cached keys: the histogram of the first (12-bit) digit is built while
+    // the keys are computed
+    if (cached) {
+      for (int i = tid; i < 4096; i += BS) s_hist[i] = 0u;
+      if (tid == 0) s_fill = 0;
+      __syncthreads();
+      for (int i = tid; i < nn; i += BS) {
+        const uint64_t k = key_of(lo + i);
+        s_keys[i] = k;
+        atomicAdd(&s_hist[(uint32_t)(k >> 52)], 1u);
+      }
+    }
     __syncthreads();
     auto key_at = [&](int i) -> uint64_t { return cached ? s_keys[i] : key_of(lo + i); };
     // Radix passes narrow the candidates (keys that match `prefix` on the bits
@@ -203,17 +213,20 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
     while (ncand > kRankMax && shift > 0) {
       const int bits = (shift == 64) ? 12 : 8;
       const int nb = 1 << bits;
+      const bool prebuilt = cached && shift == 64;
       shift -= bits;
-      for (int i = tid; i < nb; i += BS) s_hist[i] = 0u;
-      if (tid == 0) s_fill = 0;
-      __syncthreads();
       const int len = listed ? ncand : nn;
-      for (int i = tid; i < len; i += BS) {
-        const uint64_t k = listed ? s_ck[i] : key_at(i);
-        if (listed || (k & pmask) == prefix)
-          atomicAdd(&s_hist[(uint32_t)(k >> shift) & (uint32_t)(nb - 1)], 1u);
+      if (!prebuilt) {
+        for (int i = tid; i < nb; i += BS) s_hist[i] = 0u;
+        if (tid == 0) s_fill = 0;
+        __syncthreads();
+        for (int i = tid; i < len; i += BS) {
+          const uint64_t k = listed ? s_ck[i] : key_at(i);
+          if (listed || (k & pmask) == prefix)
+            atomicAdd(&s_hist[(uint32_t)(k >> shift) & (uint32_t)(nb - 1)], 1u);
+        }
+        __syncthreads();
       }
-      __syncthreads();
       // the bin that holds the need-th candidate: block-wide scan of bin groups
       {
         const int per = nb >= BS ? nb / BS : 1;
@@ -240,18 +253,23 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
       prefix |= (uint64_t)s_digit << shift;
       pmask |= (uint64_t)(nb - 1) << shift;
       if (newc <= kSelectCand) {
-        // unordered compaction of the survivors (order is irrelevant here)
+        // unordered compaction of the survivors (order is irrelevant here);
+        // straight into the list unless the list itself is being read
+        uint64_t* ck = listed ? s_ck2 : s_ck;
+        int* ci = listed ? s_ci2 : s_ci;
         for (int i = tid; i < len; i += BS) {
           const uint64_t k = listed ? s_ck[i] : key_at(i);
           if ((k & pmask) == prefix) {
             const int slot = atomicAdd(&s_fill, 1);
-            s_ck2[slot] = k;
-            s_ci2[slot] = listed ? s_ci[i] : lo + i;
+            ck[slot] = k;
+            ci[slot] = listed ? s_ci[i] : lo + i;
           }
         }
         __syncthreads();
-        for (int i = tid; i < newc; i += BS) { s_ck[i] = s_ck2[i]; s_ci[i] = s_ci2[i]; }
-        __syncthreads();
+        if (listed) {
+          for (int i = tid; i < newc; i += BS) { s_ck[i] = s_ck2[i]; s_ci[i] = s_ci2[i]; }
+          __syncthreads();
+        }
         listed = true;
       }
       ncand = newc;
