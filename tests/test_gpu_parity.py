@@ -214,6 +214,49 @@ def test_split_count_invariance_and_determinism(monkeypatch):
         assert float((o - outs[0]).abs().max()) <= 1e-2
 
 
+@pytest.mark.parametrize("cfg", ["decode", "topk", "prefill"])
+def test_step_replays_from_a_hip_graph(cfg):
+    """select + fwd captured once in a HIP graph (torch.cuda.graph records the
+    library's launches on its capture stream) replay to the eager result, bit
+    for bit, on several replays with eager work and synchronisations between
+    them (the library records no memset or host sync in these calls)."""
+    _require_gpu()
+    spec = {"decode": I.scaled_spec(2, 8, 4), "topk": I.scaled_spec(5, 32, 2),
+            "prefill": I.scaled_spec(4, 64, 2)}[cfg]
+    wl = I.build(spec)
+    print(f"[graph] {wl.spec.name}", flush=True)
+    dw = DeviceWorkload(wl)
+    if wl.spec.sel_mode == I.SEL_TOPK_MEANKEY:
+        dw.summary()
+    dw.step()
+    torch.cuda.synchronize()
+    ref_o, ref_l = dw.out.clone(), dw.lse.clone()
+    ref_ind, ref_pages = dw.selection()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        dw.step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        dw.step()
+    torch.cuda.synchronize()
+    for it in range(3):
+        dw.out.zero_()
+        dw.lse.zero_()
+        dw.sel_pages.zero_()
+        dw.sel_indptr.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dw.out, ref_o), f"replay {it}: output differs from eager"
+        assert torch.equal(dw.lse, ref_l), f"replay {it}: lse differs from eager"
+        ind, pages = dw.selection()
+        assert np.array_equal(ind, ref_ind) and np.array_equal(pages, ref_pages), f"replay {it}: selection"
+        float((dw.out.float() * 2.0).sum())   # eager work between replays
+
+
 def test_physical_placement_invariance():
     _require_gpu()
     wl = I.build(_spec(name="placement", P=32, ctx_lens=[1200, 555], q_lens=[2, 1],
