@@ -62,7 +62,10 @@
  * of bounds on bad table or list contents: an out-of-range page id, unmapped
  * segment or out-of-range physical page is skipped (contributes nothing);
  * seg_paged_attn_validate reports such data synchronously. Calls that share a
- * workspace must not overlap.
+ * workspace must not overlap. Every call except seg_paged_attn_validate only
+ * launches kernels on `stream` (no memset, no copy, no host synchronisation;
+ * the profiling hooks, when on, add event records), so a caller can capture
+ * them in a HIP graph and replay it.
  */
 #ifndef SEGPA_H
 #define SEGPA_H
