@@ -112,6 +112,14 @@ EDGE = {
                            forced_tail=1, ctx_lens=[3000, 1500], q_lens=[1, 1], sel_seed=9),
     "page128_topk": dict(P=128, seg_tokens=512, sel_mode=I.SEL_TOPK_MEANKEY, budgets=[4, 2],
                          ctx_lens=[1800, 700]),
+    # more candidate pages than the selection kernel keeps in LDS (4096): the
+    # keys are recomputed in every radix pass
+    "topk_uncached": dict(sel_mode=I.SEL_TOPK_MEANKEY, D=64, seg_tokens=4096, budgets=[300, 40],
+                          ctx_lens=[4300 * 16 + 5, 900], shift_pages=40, shift_mag=3.0,
+                          forced_tail=2),
+    "random_uncached": dict(sel_mode=I.SEL_RANDOM_HASH, D=64, seg_tokens=4096, budgets=[350, 20],
+                            ctx_lens=[4500 * 16 - 3, 700], forced_head=3, forced_tail=2,
+                            sel_seed=31),
 }
 
 
