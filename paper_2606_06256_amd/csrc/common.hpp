@@ -89,13 +89,6 @@ __device__ __forceinline__ uint64_t splitmix64(uint64_t state) {
   return splitmix64_mix(state + 0x9E3779B97F4A7C15ull);
 }
 
-// Wave-wide inclusive/exclusive counts of a predicate, in lane order.
-__device__ __forceinline__ int lane_prefix_count(uint64_t ballot) {
-  const int lane = __lane_id();
-  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-  return __popcll(ballot & below);
-}
-
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 // HBM -> LDS copy of 16 bytes per lane: bytes [voff, voff + 16) of the buffer
