@@ -265,6 +265,32 @@ def test_step_replays_from_a_hip_graph(cfg):
         float((dw.out.float() * 2.0).sum())   # eager work between replays
 
 
+def test_two_streams_run_independently():
+    """Two workloads with their own workspaces, stepped on two streams at the
+    same time (several rounds), give the results each gives alone."""
+    _require_gpu()
+    wa = I.build(I.scaled_spec(2, 8, 4))
+    wb = I.build(I.scaled_spec(4, 64, 2))      # a chunked prefill next to a decode
+    da, db = DeviceWorkload(wa), DeviceWorkload(wb)
+    da.step()
+    db.step()
+    torch.cuda.synchronize()
+    ref = [(da.out.clone(), da.lse.clone()), (db.out.clone(), db.lse.clone())]
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    for it in range(3):
+        for dw in (da, db):
+            dw.out.zero_()
+            dw.lse.zero_()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(sa):
+            da.step()
+        with torch.cuda.stream(sb):
+            db.step()
+        torch.cuda.synchronize()
+        for dw, (ro, rl) in zip((da, db), ref):
+            assert torch.equal(dw.out, ro) and torch.equal(dw.lse, rl), f"{dw.wl.spec.name} round {it}"
+
+
 def test_physical_placement_invariance():
     _require_gpu()
     wl = I.build(_spec(name="placement", P=32, ctx_lens=[1200, 555], q_lens=[2, 1],
