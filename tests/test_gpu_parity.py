@@ -104,6 +104,12 @@ EDGE = {
                                q_lens=[40, 40], ctx_lens=[900, 300]),
     "prefill_rows_g16": dict(Hq=32, Hkv=2, q_lens=[33, 17], ctx_lens=[600, 256]),
     "prefill_many_entries": dict(ctx_lens=[20000, 3000], q_lens=[40, 8], seg_tokens=4096),
+    # per-page key scales (LogNormal): scores far apart within a row, so the
+    # prefill's running reference max moves several times mid-stream
+    "prefill_scaled_keys": dict(k_page_scale_sigma=1.0, q_lens=[60, 40], ctx_lens=[1500, 700]),
+    "prefill_scaled_keys_d64": dict(D=64, k_page_scale_sigma=1.5, q_lens=[70, 35],
+                                    ctx_lens=[1200, 400], sel_mode=I.SEL_RANDOM_HASH,
+                                    budgets=[40, 20], forced_tail=5, sel_seed=13),
     # the largest page sizes: several 16-token tiles per page, partial last pages
     "page128": dict(P=128, seg_tokens=512, ctx_lens=[1000, 130]),
     "page256_d64": dict(P=256, seg_tokens=1024, D=64, ctx_lens=[2000, 257], q_lens=[3, 1]),
