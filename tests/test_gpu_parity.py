@@ -297,6 +297,24 @@ def test_two_streams_run_independently():
             assert torch.equal(dw.out, ro) and torch.equal(dw.lse, rl), f"{dw.wl.spec.name} round {it}"
 
 
+@pytest.mark.parametrize("cfg", ["decode", "prefill"])
+def test_fwd_without_lse(cfg):
+    """lse may be NULL: the output is the same as with it (decode with split
+    partials, and the chunked prefill)."""
+    _require_gpu()
+    from paper_2606_06256_amd import binding as B
+    spec = {"decode": I.scaled_spec(2, 8, 4), "prefill": I.scaled_spec(4, 64, 2)}[cfg]
+    dw = DeviceWorkload(I.build(spec))
+    dw.step()
+    torch.cuda.synchronize()
+    ref = dw.out.clone()
+    dw.out.zero_()
+    B.seg_paged_attn_fwd(dw.dims, dw.q, dw.q_indptr, dw.ctx_lens, dw.k_pool, dw.v_pool, dw.seg_table,
+                         dw.page_table, dw.sel_indptr, dw.sel_pages, dw.out, None, dw.workspace)
+    torch.cuda.synchronize()
+    assert torch.equal(dw.out, ref)
+
+
 def test_physical_placement_invariance():
     _require_gpu()
     wl = I.build(_spec(name="placement", P=32, ctx_lens=[1200, 555], q_lens=[2, 1],
