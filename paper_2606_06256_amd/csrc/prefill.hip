@@ -22,9 +22,10 @@
 // In the S^T layout each lane holds 16 keys of one row, so the row max needs
 // one cross-half swap and the running max, the sum and the rescale are
 // lane-local. The probabilities of tokens 8h..8h+7 of a tile must sit in lane
-// half h to meet V rows in token order; the S^T layout leaves half h with
-// tokens 4h..4h+3 and 8+4h..8+4h+3, so one v_permlane32_swap per register pair
-// exchanges the middle two quarters.
+// half h to meet V rows in token order. The S^T layout gives lane half h the
+// key rows 4h..4h+3 and 8+4h..8+4h+3 of each 16, so key row i of the K
+// operand holds the token whose index is i with bits 2 and 3 exchanged; the
+// probabilities then come out in V's token order with no lane exchange.
 //
 // Waves w and w + 4 share a SIMD. Waves 4..7 run half a step behind: in the
 // interval between two barriers they first finish the previous step (its
@@ -47,6 +48,11 @@ __device__ __forceinline__ f32x16 mfma32x32x16(s16x8 a, s16x8 b, f32x16 c) {
 __device__ __forceinline__ float max_halves(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// exchange of bits 2 and 3 of a key index within its 16-token tile
+__device__ __forceinline__ int swap_bits23(int i) {
+  return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1);
 }
 
 // value of lane l ^ 32
@@ -118,6 +124,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
   const int qi = (row_ok ? R : R0) / G;
   const int hh = (row_ok ? R : R0) - qi * G;
   const int vis_row = min(L - 1, L - nq + qi);          // last visible position of this row
+  const int krow = swap_bits23(j & 15);                   // token of this lane's K operand row
   const int vis_lo = min(L - 1, L - nq + R0 / G);       // smallest over the block
   const int vis_hi = min(L - 1, L - nq + (min(rows, R0 + kPfRows) - 1) / G);
 
@@ -263,7 +270,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
         const s16x8 kop = *reinterpret_cast<const s16x8*>(
-            kb + (j >> 4) * TB + (((2 * s2 + hf) * kTile + (j & 15)) * 16));
+            kb + (j >> 4) * TB + (((2 * s2 + hf) * kTile + krow) * 16));
         sacc = mfma32x32x16(kop, qreg[s2], sacc);
       }
       return sacc;
@@ -283,7 +290,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
         for (int rr = 0; rr < 16; ++rr) {
           const int kk = 8 * (rr >> 2) + 4 * hf + (rr & 3);
           const int tp = (kk < 16 ? pos0 : pos1);
-          if (!(tp >= 0 && tp + (kk & 15) <= vis_row)) sv[rr] = -INFINITY;
+          if (!(tp >= 0 && tp + swap_bits23(kk & 15) <= vis_row)) sv[rr] = -INFINITY;
         }
       }
       float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
@@ -311,7 +318,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
         const s16x8 kop = *reinterpret_cast<const s16x8*>(
-            kb + (j >> 4) * TB + (((2 * s2 + hf) * kTile + (j & 15)) * 16));
+            kb + (j >> 4) * TB + (((2 * s2 + hf) * kTile + krow) * 16));
         sn_acc = mfma32x32x16(kop, qreg[s2], sn_acc);
 #pragma unroll
         for (int e = 0; e < 16 / KS; ++e) {
@@ -327,18 +334,12 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
         for (int i = 0; i < 8; ++i) t8[i] = pv[i] + pv[i + 8];
         lsum += ((t8[0] + t8[4]) + (t8[1] + t8[5])) + ((t8[2] + t8[6]) + (t8[3] + t8[7]));
       }
-      // tile t: lo = tokens 4 hf + 0..3, hi = tokens 8 + 4 hf + 0..3; after the
-      // swap half 0 holds tokens 0..7 and half 1 tokens 8..15
+      // tile t: pv[8 t .. 8 t + 7] are tokens 8 hf + 0..7, in order
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const s16x4 lo = pack_bf16x4(pv[8 * t], pv[8 * t + 1], pv[8 * t + 2], pv[8 * t + 3]);
         const s16x4 hi = pack_bf16x4(pv[8 * t + 4], pv[8 * t + 5], pv[8 * t + 6], pv[8 * t + 7]);
-        const auto l2 = __builtin_bit_cast(uint32_t __attribute__((ext_vector_type(2))), lo);
-        const auto h2 = __builtin_bit_cast(uint32_t __attribute__((ext_vector_type(2))), hi);
-        const auto x0 = __builtin_amdgcn_permlane32_swap(l2[0], h2[0], false, false);
-        const auto x1 = __builtin_amdgcn_permlane32_swap(l2[1], h2[1], false, false);
-        const uint32_t __attribute__((ext_vector_type(4))) op = {x0[0], x1[0], x0[1], x1[1]};
-        pb[t] = __builtin_bit_cast(s16x8, op);
+        pb[t] = (s16x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       }
     };
     // O^T += V^T . P^T for step x: k-slot 8 hf + e of tile t is token 8 hf + e
