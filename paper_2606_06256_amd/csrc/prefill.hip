@@ -29,9 +29,12 @@
 //
 // Waves w and w + 4 share a SIMD. Waves 4..7 run half a step behind: in the
 // interval between two barriers they first finish the previous step (its
-// P.V product), while waves 0..3 do the vector work of the current step, so
-// the matrix cores of each SIMD have one wave's products to run while the
-// other wave computes exponentials.
+// P.V product), while waves 0..3 do the vector work of the current step. The
+// gain is small: a product that waits for the busy matrix pipe also holds
+// the SIMD's vector issue, so one wave's run of products does not overlap
+// the other wave's exponentials (all waves in step time the same within
+// noise). Vector work overlaps the products only where one wave interleaves
+// its own, as the exponentials of step s do with the scores of step s + 1.
 #include "common.hpp"
 #include "kernels.hpp"
 
