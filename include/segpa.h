@@ -192,7 +192,7 @@ spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int
                                 size_t workspace_bytes, void* stream);
 
 /*
- * Appending tokens to the head-segmented KV pool (BuildState, Section 4.5,
+ * Appending tokens to the head-segmented KV pool (BuildState, Section 4.4,
  * over the head segments of Section 4.3), with an optional refresh of the key
  * sums of every page that received a token.
  * Request r's new tokens new_indptr[r] .. new_indptr[r+1]-1 take positions
@@ -258,7 +258,7 @@ spa_status_t seg_paged_attn_page_summary(const spa_dims_t* dims, const void* k_p
 /*
  * Attention mass of the chunk tokens (the probability pass feeding
  * SelectImportantTokens, Algorithm 1; the token-importance signal of the
- * sparse FFN, Section 4.5). For token t of request r's query chunk (query
+ * sparse FFN, Section 4.4). For token t of request r's query chunk (query
  * position L_r - n_q(r) + t) and KV head g:
  *   mass[q_indptr[r] + t][g] = sum over query heads h of group g and chunk
  *     queries i >= t of exp(scale * q[i][h] . k_t - lse[i][h]),
@@ -288,7 +288,7 @@ spa_status_t seg_paged_attn_token_mass(const spa_dims_t* dims, const void* q,
 
 /*
  * SelectImportantTokens (Algorithm 1) by cumulative attention mass (Section
- * 4.5): per request, the smallest set of chunk tokens whose mass reaches tau
+ * 4.4): per request, the smallest set of chunk tokens whose mass reaches tau
  * of the chunk's total, together with the most recent `recent` tokens (the
  * keep-recent-N rule of the sparse-FFN settings, Section 5).
  * Token mass m_t = float32 sum of mass[q_indptr[r] + t][0 .. mass_cols-1] in

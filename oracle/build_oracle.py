@@ -6,7 +6,7 @@ baseline leg may import or call this module; the product path never does.
 It shares no code with the HIP library and imports nothing from it.
 
 What it follows (RedKnot, arXiv 2606.06256):
-  * Section 4.5: BuildState constructs the reusable state of cached chunks;
+  * Section 4.4: BuildState constructs the reusable state of cached chunks;
     for explicit KV pages that is the keys and values written into their
     pages (and here the page key sums the mean-key rule reads).
   * Section 4.3 and Algorithm 2 (Translate): token position t of the head

@@ -6,7 +6,7 @@ It shares no code with the HIP library and imports nothing from it.
 
 What it follows (RedKnot, arXiv 2606.06256): Algorithm 1 applies the FFN only
 to the tokens SelectImportantTokens picks from a layer's attention; Section
-4.5 describes the pick as the smallest set of tokens whose cumulative
+4.4 describes the pick as the smallest set of tokens whose cumulative
 attention mass exceeds a threshold tau, and the experiments (Section 5) also
 always keep the most recent N tokens; the denoising study reports the minimum
 fraction of tokens that covers 99% of the attention mass.

@@ -1,7 +1,7 @@
 // Building head-segmented KV state: appending new tokens' keys and values to
 // their pages, then refreshing the key sums of the pages that changed.
 //
-// What is computed: Section 4.5 (BuildState builds the reusable state of a
+// What is computed: Section 4.4 (BuildState builds the reusable state of a
 // chunk) over the head-segmented pages of Section 4.3. Request r's new tokens
 // take positions ctx_lens[r], ctx_lens[r] + 1, ... of every KV head's stream;
 // position t is slot t % P of logical page t / P, which Algorithm 2's

@@ -1,5 +1,5 @@
 // Attention-mass token selection (SelectImportantTokens of Algorithm 1; the
-// cumulative-mass rule of Section 4.5, with the keep-recent-N window of the
+// cumulative-mass rule of Section 4.4, with the keep-recent-N window of the
 // sparse-FFN settings in Section 5).
 //
 // Two kernels.

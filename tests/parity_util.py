@@ -33,18 +33,26 @@ LSE_ABS = 1e-3
 TIE_REL = 1e-12
 
 
-_KV_CACHE: dict = {}
+KV_CACHE_UNITS = 6
 
 
 def kv64(wl: I.Workload, r: int, g: int):
-    """Logical K, V of unit (r, g) as float64, generated on the CPU (small cache)."""
-    key = (id(wl), r, g)
-    if key not in _KV_CACHE:
-        if len(_KV_CACHE) >= 6:
-            _KV_CACHE.pop(next(iter(_KV_CACHE)))
+    """Logical K, V of unit (r, g) as float64, generated on the CPU.
+
+    The cache lives on the workload object itself, so its entries die with the
+    workload: a later workload can never read an earlier one's keys (object
+    ids are reused after garbage collection, so an id-keyed global cache
+    could return another workload's arrays). At most KV_CACHE_UNITS units
+    are held per workload.
+    """
+    cache = wl.__dict__.setdefault("_kv64_cache", {})
+    key = (r, g)
+    if key not in cache:
+        if len(cache) >= KV_CACHE_UNITS:
+            cache.pop(next(iter(cache)))
         K, V = wl.unit_kv(r, g, "cpu")
-        _KV_CACHE[key] = (K.double().numpy(), V.double().numpy())
-    return _KV_CACHE[key]
+        cache[key] = (K.double().numpy(), V.double().numpy())
+    return cache[key]
 
 
 def oracle_selection(wl: I.Workload, q64: np.ndarray, units=None) -> dict:

@@ -1,4 +1,4 @@
-"""Pins of the KV append / key-sum refresh oracle (Sections 4.3, 4.5) against
+"""Pins of the KV append / key-sum refresh oracle (Sections 4.3, 4.4) against
 the independently pinned pool reader and key-sum definition."""
 import numpy as np
 import pytest

@@ -13,8 +13,7 @@ pytestmark = pytest.mark.gpu
 
 
 def _require_gpu():
-    if not torch.cuda.is_available():
-        pytest.skip("needs a GPU")
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
 
 
 def _pool(D, P, n_phys, seed):

@@ -462,3 +462,54 @@ def test_aliased_segments_read_the_same_pages():
 def test_translate_rejects_unmapped_segment():
     with pytest.raises(ValueError):
         O.translate([3, -1], [0, 1, 2, 3, 4, 5, 6, 7], 2, 2)
+
+
+def test_forward_unit_bruteforce_gqa_rows_and_default_scale():
+    """forward_unit against pure-Python loops over the whole call's layout.
+
+    Two requests with ragged query chunks (so request 1's rows start at a
+    nonzero offset of q_indptr), Hq = 8 query heads over Hkv = 2 KV heads
+    (G = 4). Query head h must read KV head h // G (contiguous groups), its
+    rows must be q_indptr[r] .. q_indptr[r+1]-1, and the default scale must
+    be 1/sqrt(D). Each KV head has its own keys, so a wrong head map, a wrong
+    row offset or another scale changes the result.
+    """
+    P, D, Hq, Hkv = 16, 8, 8, 2
+    G = Hq // Hkv
+    ctx = [45, 70]
+    q_lens = [3, 5]
+    q_indptr = np.array([0, 3, 8])
+    r0 = _rng(4242)
+    q_all = _bf16(r0.standard_normal((8, Hq, D)))
+    KV = {(r, g): (_bf16(r0.standard_normal((ctx[r], D))), _bf16(r0.standard_normal((ctx[r], D))))
+          for r in range(2) for g in range(Hkv)}
+    pages = {(0, 0): [0, 2], (0, 1): [1, 2], (1, 0): [0, 3, 4], (1, 1): [2, 4]}
+    scale = 1.0 / math.sqrt(D)
+    for r in range(2):
+        L, n_q = ctx[r], q_lens[r]
+        for h in range(Hq):
+            kv = h // G                                # the head map under test
+            K, V = KV[(r, kv)]
+            Oo, LSE = O.forward_unit(q_all, q_indptr, np.array(ctx), Hq, Hkv, P, r * Hkv + kv,
+                                     pages[(r, kv)], K, V)
+            assert Oo.shape == (n_q, G, D) and LSE.shape == (n_q, G)
+            for i in range(n_q):
+                row = int(q_indptr[r]) + i
+                pos = L - n_q + i
+                toks = [t for p in pages[(r, kv)] for t in range(p * P, p * P + P)
+                        if t < L and t <= pos]
+                if not toks:
+                    assert LSE[i, h % G] == -math.inf
+                    continue
+                s = []
+                for t in toks:
+                    acc = 0.0
+                    for d in range(D):
+                        acc += q_all[row, h, d] * K[t, d]
+                    s.append(scale * acc)
+                m = max(s)
+                z = sum(math.exp(x - m) for x in s)
+                for d in range(D):
+                    o = sum(math.exp(x - m) * V[t, d] for x, t in zip(s, toks)) / z
+                    assert abs(o - Oo[i, h % G, d]) < 1e-12
+                assert abs(m + math.log(z) - LSE[i, h % G]) < 1e-12
