@@ -2,19 +2,25 @@
 
 A step is one pass of the hot path over one batch of synthetic input: page
 selection (seg_paged_attn_select) and the attention forward with its split
-combine (seg_paged_attn_fwd). The default workload is the Llama-3-8B-shaped
-sparse decode: 16 requests, 32 query / 8 KV heads, head dim 128, 32K context
-in 2048-token segments, page 16, 25% of the pages of every KV head selected
-(first and last segment included).
+combine (seg_paged_attn_fwd). The default workload is the largest
+single-GPU decode: the variable-length sparse decode (64 requests, 32 query /
+8 KV heads, head dim 128, contexts log-uniform in [4096, 131072] tokens in
+4096-token segments, page 16, a per-request budget of 5-50% of the pages,
+keys of each page scaled by LogNormal(0, 0.5)).
 
 Output: one JSON line. `value` is attended KV tokens per second for the whole
 step (inputs resident in HBM). `roofline` is the dominant kernel
 (decode_attn): algorithmic bytes per launch over its mean launch time,
-measured with HIP events on the launch stream. `cpu_baseline` is the fp64
-oracle timed on this host's cores (a pool of single-threaded processes) on
-a sample of the same step.
+measured with HIP events attached to each dispatch on the launch stream.
+`cpu_baseline` is the fp64 oracle timed on this host's cores (a pool of
+single-threaded processes) on a sample of the same step.
+`config.sub_records` holds the same measurement, from the same run, for the
+Llama-3-8B-shaped decode (2), the chunked prefill (4, matrix-core bound) and
+the top-k selection + attention workload (5, with its page-summary build
+timed on its own).
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N] [--no-cpu-baseline]
+                [--sub-records 2,4,5 | --no-sub-records]
 """
 from __future__ import annotations
 
@@ -491,8 +497,12 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=None,
-                    help="named workload 1..9 (default 2; 9 for --op token_mass)")
+                    help="named workload 1..9 (default 3, the varlen sparse decode; 9 for --op token_mass)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sub-records", default="2,4,5",
+                    help="workloads also measured in the same run (step time, dominant-kernel "
+                         "roofline), reported under config.sub_records")
+    ap.add_argument("--no-sub-records", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (scale for HBM byte counters)")
     ap.add_argument("--op", choices=["step", "rope_align", "append", "token_mass"], default="step",
@@ -509,7 +519,7 @@ def main():
     ap.add_argument("--calib-write")
     args = ap.parse_args()
     if args.workload is None:
-        args.workload = 9 if args.op == "token_mass" else 2
+        args.workload = 9 if args.op == "token_mass" else 3
     if args.record_traffic:
         args.kernel = args.record_traffic
         write_traffic_entry(args)
@@ -549,12 +559,53 @@ def main():
 
     import torch
     from paper_2606_06256_amd import binding, build_lib
-    from paper_2606_06256_amd.device import DeviceWorkload
     if not os.path.exists(binding.LIB_PATH):
         build_lib.build()
     if not torch.cuda.is_available():
         raise RuntimeError("bench.py needs a GPU")
     torch.cuda.set_device(0)
+
+    head = measure_step(wl, args, torch, binding, cold=True, with_copy=True)
+    subs = []
+    if not args.no_sub_records:
+        for i in [int(x) for x in args.sub_records.split(",") if x.strip()]:
+            if i == args.workload:
+                continue
+            torch.cuda.empty_cache()
+            r = measure_step(I.config(i), args, torch, binding, cold=False, with_copy=False)
+            subs.append({k: r[k] for k in ("ms_per_step", "value", "unit")} |
+                        {"workload": r["config"]["workload"], "roofline": r["roofline"],
+                         "kernels": r["config"]["kernels"],
+                         "attended_kv_tokens_per_step": r["config"]["attended_kv_tokens_per_step"]} |
+                        ({"page_summary_ms": r["config"]["page_summary_ms"]}
+                         if "page_summary_ms" in r["config"] else {}))
+    line = {
+        "metric": METRIC,
+        "value": head["value"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "cpu_baseline": cpu,
+    }
+    if subs:
+        line["config"]["sub_records"] = subs
+    print(json.dumps(line), flush=True)
+
+
+def measure_step(wl, args, torch, binding, *, cold, with_copy):
+    """Warm-up, then exactly args.steps timed steps of `wl` (inputs resident in
+    HBM), then the same number of steps with per-kernel dispatch timing."""
+    from paper_2606_06256_amd import inputs as I
+    from paper_2606_06256_amd.device import DeviceWorkload
 
     dw = DeviceWorkload(wl)
     summary_ms = None
@@ -586,7 +637,8 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(stop) / args.steps
 
-    # per-kernel launch times (HIP events around each launch, on its stream)
+    # per-kernel launch times: HIP events attached to each kernel dispatch on
+    # the stream it is launched on (the kernel's own start and end)
     binding.profile_begin()
     for _ in range(args.steps):
         dw.step()
@@ -611,41 +663,29 @@ def main():
         roofline = {"kernel": kname, "bound": "hbm", "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": traffic, "bytes_per_launch": abytes, "launch_ms": round(attn_ms, 5)}
+    roofline["launch_timing"] = "HIP events attached to the kernel dispatch"
     if traffic is not None:
         roofline["traffic_over_algorithmic_bytes"] = round(traffic / abytes, 4)
-    if not prefill:
+        roofline["traffic_source"] = ("recorded rocprofv3 FETCH_SIZE/WRITE_SIZE passes "
+                                      "(profiles/hbm_traffic.json), valid for the current kernel sources")
+    if with_copy and not prefill:
         copy = device_copy_gbs(torch)
         roofline["measured_device_copy_gbs"] = round(copy, 1)
         roofline["frac_of_measured_device_copy"] = round(achieved / copy, 4)
     kernels = {k: {"launches": n, "mean_ms": round(t / n, 5)} for k, (n, t) in prof.items()}
-    cold = cold_steps(dw, torch, binding, kname)
-    line = {
-        "metric": METRIC,
-        "value": round(tokens / (ms_per_step * 1e-3), 1),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": wl.spec.name, "description": wl.spec.description,
-                   "requests": wl.B, "q_heads": wl.Hq, "kv_heads": wl.Hkv, "head_dim": wl.D,
-                   "page_size": wl.P, "segment_tokens": wl.spec.seg_tokens,
-                   "attended_kv_tokens_per_step": tokens,
-                   "step_gbs": round(abytes / (ms_per_step * 1e-3) / 1e9, 1),
-                   "kernels": kernels},
-        "roofline": roofline,
-        "cpu_baseline": cpu,
-    }
-    line["config"]["cold_cache"] = cold
+    config = {"workload": wl.spec.name, "description": wl.spec.description,
+              "requests": wl.B, "q_heads": wl.Hq, "kv_heads": wl.Hkv, "head_dim": wl.D,
+              "page_size": wl.P, "segment_tokens": wl.spec.seg_tokens,
+              "attended_kv_tokens_per_step": tokens,
+              "step_gbs": round(abytes / (ms_per_step * 1e-3) / 1e9, 1),
+              "kernels": kernels}
+    if cold:
+        config["cold_cache"] = cold_steps(dw, torch, binding, kname)
     if summary_ms is not None:
-        line["config"]["page_summary_ms"] = round(summary_ms, 4)
-    print(json.dumps(line), flush=True)
-
+        config["page_summary_ms"] = round(summary_ms, 4)
+    del dw
+    return {"value": round(tokens / (ms_per_step * 1e-3), 1), "unit": "tokens/s",
+            "ms_per_step": round(ms_per_step, 5), "config": config, "roofline": roofline}
 
 if __name__ == "__main__":
     main()

@@ -22,6 +22,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // ---- launch timing (opt-in measurement aid) ---------------------------------
+thread_local LaunchEvents t_launch_events;
 struct ProfRecord {
   const char* name;
   hipEvent_t start, stop;
@@ -44,9 +45,12 @@ hipError_t timed_launch(const char* name, hipStream_t stream, F&& launch) {
     (void)hipEventDestroy(a);
     return hipErrorUnknown;
   }
-  (void)hipEventRecord(a, stream);
+  // the events ride on the dispatch (start and end of the kernel itself)
+  LaunchEvents& ev = launch_events();
+  ev.start = a;
+  ev.stop = b;
   const hipError_t e = launch();
-  (void)hipEventRecord(b, stream);
+  ev.start = ev.stop = nullptr;
   std::lock_guard<std::mutex> lk(g_prof_mu);
   g_prof.push_back({name, a, b});
   return e;
@@ -101,8 +105,10 @@ spa_status_t check_dims(const spa_dims_t* d) {
   if (d->page_size < 16 || d->page_size > 256 || !is_pow2(d->page_size)) return SPA_ERR_UNSUPPORTED;
   const int64_t units = (int64_t)d->num_requests * d->num_kv_heads;
   if (units > SPA_MAX_UNITS) return SPA_ERR_UNSUPPORTED;
+  // both factors are positive int32, so max_pages < 2^62; P is a power of two,
+  // so max_pages * P < 2^31 exactly when max_pages < 2^31 / P (no overflow)
   const int64_t max_pages = (int64_t)d->max_segments * d->pages_per_segment;
-  if (max_pages * d->page_size >= (int64_t(1) << 31)) return SPA_ERR_UNSUPPORTED;
+  if (max_pages >= (int64_t(1) << 31) / d->page_size) return SPA_ERR_UNSUPPORTED;
   if (units * max_pages >= (int64_t(1) << 31)) return SPA_ERR_UNSUPPORTED;
   if (d->num_phys_pages >= (int64_t(1) << 31) || d->num_virtual_pages >= (int64_t(1) << 31))
     return SPA_ERR_UNSUPPORTED;
@@ -141,6 +147,8 @@ size_t select_workspace(const spa_dims_t* d, int32_t mode) {
 spa_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPA_OK : SPA_ERR_HIP; }
 
 }  // namespace
+
+LaunchEvents& segpa::launch_events() { return t_launch_events; }
 
 extern "C" {
 
@@ -319,7 +327,9 @@ spa_status_t seg_paged_attn_append(const spa_dims_t* dims, const int32_t* ctx_le
                                    float* page_ksum, void* stream) {
   const spa_status_t st = check_dims(dims);
   if (st != SPA_OK) return st;
-  if (n_new < 0 || n_new * dims->num_kv_heads >= (int64_t(1) << 31) / 16) return SPA_ERR_INVALID_ARG;
+  // n_new * Hkv < 2^27 (tiles of new tokens stay in 31 bits), tested without
+  // forming the product: n_new * Hkv <= 2^27 - 1 exactly when n_new <= (2^27 - 1) / Hkv
+  if (n_new < 0 || n_new > ((int64_t(1) << 27) - 1) / dims->num_kv_heads) return SPA_ERR_INVALID_ARG;
   if (n_new > 0 && (ctx_lens == nullptr || new_indptr == nullptr || k_new == nullptr ||
                     v_new == nullptr || seg_table == nullptr || page_table == nullptr ||
                     k_pool == nullptr || v_pool == nullptr))
@@ -509,7 +519,10 @@ spa_status_t seg_paged_attn_validate(const spa_dims_t* dims, const int32_t* ctx_
 }
 
 const char* seg_paged_attn_status_string(spa_status_t status) {
-  switch (status) {
+  // a C caller may pass any int: read the raw value rather than the enum
+  int32_t code;
+  std::memcpy(&code, &status, sizeof code);
+  switch (code) {
     case SPA_OK: return "ok";
     case SPA_ERR_INVALID_ARG: return "invalid argument";
     case SPA_ERR_UNSUPPORTED: return "unsupported shape or parameter";

@@ -109,10 +109,16 @@ __global__ __launch_bounds__(256) void key_refresh_kernel(const AppendArgs a) {
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
   if (a.n_new <= 0) return hipSuccess;
   const dim3 grid((unsigned)((a.n_new + kTile - 1) / kTile), (unsigned)a.Hkv);
-  hipLaunchKernelGGL(append_kernel, grid, dim3(256), 0, stream, a);
+  // timed as one call: the start event on the first dispatch, the stop event
+  // on the last
+  const LaunchEvents ev = launch_events();
+  const bool refresh = a.page_ksum != nullptr;
+  launch_with_events(append_kernel, grid, dim3(256), 0, stream, ev.start,
+                     refresh ? nullptr : ev.stop, a);
   const hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.page_ksum == nullptr) return e;
-  hipLaunchKernelGGL(key_refresh_kernel, dim3((unsigned)(a.B * a.Hkv), 8), dim3(256), 0, stream, a);
+  if (e != hipSuccess || !refresh) return e;
+  launch_with_events(key_refresh_kernel, dim3((unsigned)(a.B * a.Hkv), 8), dim3(256), 0, stream,
+                     nullptr, ev.stop, a);
   return hipGetLastError();
 }
 

@@ -380,18 +380,18 @@ hipError_t launch_decode(const FwdArgs& a, hipStream_t stream) {
   const size_t lds = (size_t)(a.units + 1) * sizeof(int32_t);
   const dim3 grid(a.total_waves / (kDecodeBlock / kWave)), block(kDecodeBlock);
   if (a.D == 128)
-    hipLaunchKernelGGL(decode_attn_kernel<128>, grid, block, lds, stream, a);
+    launch(decode_attn_kernel<128>, grid, block, lds, stream, a);
   else
-    hipLaunchKernelGGL(decode_attn_kernel<64>, grid, block, lds, stream, a);
+    launch(decode_attn_kernel<64>, grid, block, lds, stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_combine(const FwdArgs& a, hipStream_t stream) {
   const dim3 grid(a.units * a.row_blocks), block(256);
   if (a.D == 128)
-    hipLaunchKernelGGL(combine_kernel<128>, grid, block, 0, stream, a);
+    launch(combine_kernel<128>, grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL(combine_kernel<64>, grid, block, 0, stream, a);
+    launch(combine_kernel<64>, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

@@ -1,10 +1,39 @@
 // Kernel argument blocks and host-side launchers (internal to libsegpa.so).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace segpa {
+
+// Optional dispatch timing. While the library's timing hooks are on, the host
+// code sets these events (per host thread) before a launcher runs. They are
+// attached to the kernel dispatch itself, so their elapsed time is the
+// kernel's own execution: an event recorded beside a launch would add the
+// time between that marker and the dispatch. With no events set, kernels
+// launch as plain dispatches.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+template <typename F, typename... Args>
+inline void launch_with_events(F kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               hipEvent_t start, hipEvent_t stop, Args... args) {
+  if (start == nullptr && stop == nullptr)
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+  else
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, start, stop, 0u, args...);
+}
+
+// One kernel dispatch, timed by the current launch events if any are set.
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, Args... args) {
+  const LaunchEvents ev = launch_events();
+  launch_with_events(kernel, grid, block, lds, s, ev.start, ev.stop, args...);
+}
 
 constexpr int kTile = 16;       // tokens per KV tile; a page holds P / 16 tiles
 constexpr int kWave = 64;

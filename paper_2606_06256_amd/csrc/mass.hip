@@ -350,9 +350,9 @@ __global__ __launch_bounds__(kTokBlock) void select_tokens_kernel(const TokSelAr
 hipError_t launch_token_mass(const MassArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)((int64_t)a.B * a.Hkv * a.key_groups)), block(kMassThreads);
   if (a.D == 128)
-    hipLaunchKernelGGL(token_mass_kernel<128>, grid, block, 0, stream, a);
+    launch(token_mass_kernel<128>, grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL(token_mass_kernel<64>, grid, block, 0, stream, a);
+    launch(token_mass_kernel<64>, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 
@@ -361,11 +361,11 @@ int token_mass_keys_per_block() { return kMassKeys; }
 hipError_t launch_select_tokens(const TokSelArgs& a, hipStream_t stream) {
   const dim3 grid(a.B), block(kTokBlock);
   if (a.max_q_len <= 1024)
-    hipLaunchKernelGGL(select_tokens_kernel<1024>, grid, block, 0, stream, a);
+    launch(select_tokens_kernel<1024>, grid, block, 0, stream, a);
   else if (a.max_q_len <= 4096)
-    hipLaunchKernelGGL(select_tokens_kernel<4096>, grid, block, 0, stream, a);
+    launch(select_tokens_kernel<4096>, grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL(select_tokens_kernel<kTokSelMax>, grid, block, 0, stream, a);
+    launch(select_tokens_kernel<kTokSelMax>, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

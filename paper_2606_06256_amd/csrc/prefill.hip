@@ -436,9 +436,9 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
 hipError_t launch_prefill(const FwdArgs& a, hipStream_t stream) {
   const dim3 grid(a.units * a.row_blocks), block(kPfThreads);
   if (a.D == 128)
-    hipLaunchKernelGGL(prefill_kernel<128>, grid, block, 0, stream, a);
+    launch(prefill_kernel<128>, grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL(prefill_kernel<64>, grid, block, 0, stream, a);
+    launch(prefill_kernel<64>, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

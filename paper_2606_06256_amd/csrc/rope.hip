@@ -149,9 +149,9 @@ hipError_t launch_rope_align(const RopeArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)((a.n + ppb - 1) / ppb)), block(kRopeBlock);
   const size_t lds = (size_t)ppb * (a.D / 2) * 2 * sizeof(double);
   if (a.D == 128)
-    hipLaunchKernelGGL(rope_align_kernel<128>, grid, block, lds, stream, a, ppb);
+    launch(rope_align_kernel<128>, grid, block, lds, stream, a, ppb);
   else
-    hipLaunchKernelGGL(rope_align_kernel<64>, grid, block, lds, stream, a, ppb);
+    launch(rope_align_kernel<64>, grid, block, lds, stream, a, ppb);
   return hipGetLastError();
 }
 

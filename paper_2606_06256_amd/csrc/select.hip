@@ -441,13 +441,13 @@ __global__ __launch_bounds__(256) void select_score_kernel(const SelArgs a) {
 
 hipError_t launch_select_scores(const SelArgs& a, hipStream_t stream) {
   const dim3 grid((a.max_pages + 255) / 256, a.units), block(256);
-  hipLaunchKernelGGL(select_score_kernel, grid, block, 0, stream, a);
+  launch(select_score_kernel, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_select_fill(const SelArgs& a, hipStream_t stream) {
   const dim3 grid(a.units), block(kSelectBlock);
-  hipLaunchKernelGGL(select_fill_kernel, grid, block, 0, stream, a);
+  launch(select_fill_kernel, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

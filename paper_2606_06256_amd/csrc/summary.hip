@@ -45,7 +45,7 @@ __global__ __launch_bounds__(256) void page_summary_kernel(const SummaryArgs a) 
 hipError_t launch_page_summary(const SummaryArgs& a, hipStream_t stream) {
   const int64_t threads = a.n_phys * (a.D / 8);
   const int64_t blocks = (threads + 255) / 256;
-  hipLaunchKernelGGL(page_summary_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+  launch(page_summary_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -87,7 +87,7 @@ __global__ __launch_bounds__(256) void validate_kernel(const ValidateArgs a) {
 }
 
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(validate_kernel, dim3(a.units), dim3(256), 0, stream, a);
+  launch(validate_kernel, dim3(a.units), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

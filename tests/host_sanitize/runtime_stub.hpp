@@ -1,0 +1,13 @@
+// Controls of the host-only HIP stand-ins (see runtime_stub.cpp).
+#pragma once
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+
+namespace stub {
+extern std::vector<std::string> launches;  // kernel kinds "launched", in order
+extern hipError_t launch_result;           // what every stub launcher returns
+extern bool validate_reports_bad;          // the validate stub reports a bad page
+extern int cus;                            // compute units reported by the device query
+}  // namespace stub
