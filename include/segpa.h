@@ -5,7 +5,8 @@
  * pointer; every size and scalar is host data. The library never allocates,
  * frees or retains caller memory past a call, except that the optional
  * profiling hooks keep host-side event records between
- * seg_paged_attn_profile_begin and seg_paged_attn_profile_end.
+ * seg_paged_attn_profile_begin and seg_paged_attn_profile_end. Its only device
+ * memory of its own is the static scratch of seg_paged_attn_fwd_noalloc.
  *
  * What is computed follows RedKnot (arXiv 2606.06256):
  *   - Section 4.3 and Algorithm 2 (SegPagedAttention): the KV cache of one
@@ -190,6 +191,32 @@ spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int
                                 const int32_t* sel_indptr, const int32_t* sel_pages,
                                 int64_t sel_capacity, void* out, float* lse, void* workspace,
                                 size_t workspace_bytes, void* stream);
+
+/*
+ * seg_paged_attn_fwd for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops or harnesses that forbid hipMalloc):
+ * the same arguments, outputs, kernels and errors, minus workspace and
+ * workspace_bytes. The split-KV partials go to a scratch array inside the
+ * library instead: SPA_NOALLOC_SCRATCH_BYTES of device memory on each GPU the
+ * call runs on (a static device array of the library's code object, present
+ * on a GPU once the library's code is loaded there, at the latest by the first
+ * call, and held until the process ends). The call allocates nothing. A shape whose partials need more than that returns
+ * SPA_ERR_WORKSPACE before anything is launched: the decode path needs
+ * (W + B * Hkv * ceil(max_q_len * G / 16)) * (16 * D + 16) * 4 bytes (rounded
+ * up to 256 twice), with W = 4 waves per compute unit (1024 on MI355X), e.g.
+ * up to about 3,000 (unit, 16-row block) pairs at D = 128; the chunked-prefill
+ * path keeps no partials. The scratch is not cleared: no call reads what an
+ * earlier call left there. All calls on one GPU share that GPU's scratch, so
+ * calls that overlap in time on one GPU (other streams, other host threads)
+ * race; the caller must order them, e.g. on one stream.
+ */
+#define SPA_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+spa_status_t seg_paged_attn_fwd_noalloc(const spa_dims_t* dims, const void* q,
+                                        const int32_t* q_indptr, const int32_t* ctx_lens,
+                                        const void* k_pool, const void* v_pool,
+                                        const int32_t* seg_table, const int32_t* page_table,
+                                        const int32_t* sel_indptr, const int32_t* sel_pages,
+                                        int64_t sel_capacity, void* out, float* lse, void* stream);
 
 /*
  * Appending tokens to the head-segmented KV pool (BuildState, Section 4.4,

@@ -16,6 +16,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsegpa.so")
 
 SPA_OK = 0
+SPA_ERR_WORKSPACE = -3
+SPA_NOALLOC_SCRATCH_BYTES = 32 << 20
 SPA_SEL_ALL, SPA_SEL_HEAD_CLASS, SPA_SEL_RANDOM_HASH, SPA_SEL_TOPK_MEANKEY = 0, 1, 2, 3
 
 
@@ -64,6 +66,9 @@ def lib() -> ctypes.CDLL:
     L.seg_paged_attn_fwd.restype = ctypes.c_int
     L.seg_paged_attn_fwd.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                      ctypes.c_int64, _P, _P, _P, ctypes.c_size_t, _P]
+    L.seg_paged_attn_fwd_noalloc.restype = ctypes.c_int
+    L.seg_paged_attn_fwd_noalloc.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P, _P, _P, _P,
+                                             _P, _P, ctypes.c_int64, _P, _P, _P]
     L.seg_paged_attn_page_summary.restype = ctypes.c_int
     L.seg_paged_attn_page_summary.argtypes = [ctypes.POINTER(spa_dims_t), _P, _P, _P, _P]
     L.seg_paged_attn_append.restype = ctypes.c_int
@@ -166,6 +171,19 @@ def seg_paged_attn_fwd(dims: spa_dims_t, q, q_indptr, ctx_lens, k_pool, v_pool, 
         _ptr(out, torch.bfloat16, "out"), _ptr(lse, torch.float32, "lse"),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
     _check("seg_paged_attn_fwd", st)
+
+
+def seg_paged_attn_fwd_noalloc(dims: spa_dims_t, q, q_indptr, ctx_lens, k_pool, v_pool, seg_table,
+                               page_table, sel_indptr, sel_pages, out, lse, stream=None):
+    """seg_paged_attn_fwd over the library's own per-GPU scratch (no workspace)."""
+    st = lib().seg_paged_attn_fwd_noalloc(
+        ctypes.byref(dims), _ptr(q, torch.bfloat16, "q"), _ptr(q_indptr, torch.int32, "q_indptr"),
+        _ptr(ctx_lens, torch.int32, "ctx_lens"), _ptr(k_pool, torch.bfloat16, "k_pool"),
+        _ptr(v_pool, torch.bfloat16, "v_pool"), _ptr(seg_table, torch.int32, "seg_table"),
+        _ptr(page_table, torch.int32, "page_table"), _ptr(sel_indptr, torch.int32, "sel_indptr"),
+        _ptr(sel_pages, torch.int32, "sel_pages"), sel_pages.numel(),
+        _ptr(out, torch.bfloat16, "out"), _ptr(lse, torch.float32, "lse"), _stream(stream))
+    _check("seg_paged_attn_fwd_noalloc", st)
 
 
 def seg_paged_attn_page_summary(dims: spa_dims_t, k_pool, page_valid_tokens, page_ksum, stream=None):

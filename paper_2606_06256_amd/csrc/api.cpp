@@ -16,6 +16,13 @@
 
 using namespace segpa;
 
+// Device scratch of seg_paged_attn_fwd_noalloc (split-KV partials). Each GPU
+// the library runs on holds its own copy until the process ends. In host
+// code `scratch` names a host-side stand-in, never the device memory: its
+// device address comes from hipGetSymbolAddress (once per device, below).
+static constexpr size_t kNoAllocScratchBytes = SPA_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -131,9 +138,14 @@ int log2i(int x) {
   return l;
 }
 
+bool is_prefill(const spa_dims_t* d) {
+  return (int64_t)d->max_q_len * (d->num_q_heads / d->num_kv_heads) >= kPrefillMinRows;
+}
+
 size_t fwd_workspace(const spa_dims_t* d) {
   const int waves = decode_waves(d->head_dim, (int)units_of(d));
   if (waves < 0) return 0;
+  if (is_prefill(d)) return kAlign;  // the chunked-prefill kernel keeps no split partials
   const int64_t slots = waves + units_of(d) * row_blocks_of(d);
   return align_up((size_t)slots * 16 * d->head_dim * sizeof(float)) +
          align_up((size_t)slots * 16 * sizeof(float));
@@ -145,6 +157,26 @@ size_t select_workspace(const spa_dims_t* d, int32_t mode) {
 }
 
 spa_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPA_OK : SPA_ERR_HIP; }
+
+// Device address of the current GPU's scratch, looked up on the first call on
+// that device (with it current) and kept per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+spa_status_t scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return SPA_ERR_HIP;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr)
+      return SPA_ERR_HIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return SPA_OK;
+}
 
 }  // namespace
 
@@ -284,20 +316,40 @@ spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int
   const float scale = dims->softmax_scale > 0.f ? dims->softmax_scale
                                                 : 1.0f / std::sqrt((float)dims->head_dim);
   a.scale_log2 = scale * kLog2e;
-  const int64_t slots = a.total_waves + (int64_t)units * a.row_blocks;
-  a.part_o = static_cast<float*>(workspace);
-  a.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                        align_up((size_t)slots * 16 * a.D * sizeof(float)));
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t rows = (int64_t)dims->max_q_len * a.G;
-  if (rows >= kPrefillMinRows) {
+  if (is_prefill(dims)) {
     // chunked prefill: one block per (unit, row block), all selected keys, no split
     a.row_blocks = (int)((rows + prefill_rows_per_block() - 1) / prefill_rows_per_block());
     return hip_status(timed_launch("prefill_attn", s, [&] { return launch_prefill(a, s); }));
   }
+  const int64_t slots = a.total_waves + (int64_t)units * a.row_blocks;
+  a.part_o = static_cast<float*>(workspace);
+  a.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                        align_up((size_t)slots * 16 * a.D * sizeof(float)));
   st = hip_status(timed_launch("decode_attn", s, [&] { return launch_decode(a, s); }));
   if (st != SPA_OK) return st;
   return hip_status(timed_launch("combine", s, [&] { return launch_combine(a, s); }));
+}
+
+spa_status_t seg_paged_attn_fwd_noalloc(const spa_dims_t* dims, const void* q,
+                                        const int32_t* q_indptr, const int32_t* ctx_lens,
+                                        const void* k_pool, const void* v_pool,
+                                        const int32_t* seg_table, const int32_t* page_table,
+                                        const int32_t* sel_indptr, const int32_t* sel_pages,
+                                        int64_t sel_capacity, void* out, float* lse, void* stream) {
+  const spa_status_t st = check_dims(dims);
+  if (st != SPA_OK) return st;
+  const size_t need = fwd_workspace(dims);
+  if (need == 0) return SPA_ERR_HIP;
+  if (need > kNoAllocScratchBytes) return SPA_ERR_WORKSPACE;
+  void* ws = nullptr;
+  const spa_status_t sst = scratch_of_current_device(&ws);
+  if (sst != SPA_OK) return sst;
+  // the same checks and kernels as seg_paged_attn_fwd, over the built-in scratch
+  return seg_paged_attn_fwd(dims, q, q_indptr, ctx_lens, k_pool, v_pool, seg_table, page_table,
+                            sel_indptr, sel_pages, sel_capacity, out, lse, ws,
+                            kNoAllocScratchBytes, stream);
 }
 
 spa_status_t seg_paged_attn_page_summary(const spa_dims_t* dims, const void* k_pool,

@@ -508,7 +508,56 @@ static void status_and_profile_paths() {
   EXPECT(seg_paged_attn_profile_end(nullptr, nullptr, nullptr, 0) == 0);
 }
 
+static void noalloc_paths() {
+  // the first lookup of the built-in scratch fails: reported, nothing launched
+  spa_dims_t d = dims();
+  auto call = [&](const spa_dims_t& dd, const void* q = A, void* out = A2) {
+    return seg_paged_attn_fwd_noalloc(&dd, q, I32, I32, A, A2, I32, I32, I32, I32, 1 << 20, out,
+                                      (float*)A, nullptr);
+  };
+  reset();
+  stub::symbol_lookup_fails = true;
+  EXPECT_ST(call(d), SPA_ERR_HIP);
+  EXPECT(stub::launches.empty());
+  stub::symbol_lookup_fails = false;
+  // then found once and kept for the device
+  EXPECT_ST(call(d), SPA_OK);
+  EXPECT(launched({"decode_attn", "combine"}));
+  const float* first = stub::last_part_o;
+  EXPECT(first != nullptr);
+  const int lookups = stub::symbol_lookups;
+  reset();
+  EXPECT_ST(call(d), SPA_OK);
+  EXPECT(stub::symbol_lookups == lookups);
+  EXPECT(stub::last_part_o == first);
+  // the same argument checks as seg_paged_attn_fwd
+  EXPECT_ST(call(d, nullptr), SPA_ERR_INVALID_ARG);
+  EXPECT_ST(call(d, A, nullptr), SPA_ERR_INVALID_ARG);
+  EXPECT_ST(call(d, MIS16), SPA_ERR_INVALID_ARG);
+  spa_dims_t bad = d;
+  bad.head_dim = 48;
+  EXPECT_ST(call(bad), SPA_ERR_UNSUPPORTED);
+  EXPECT_ST(seg_paged_attn_fwd_noalloc(nullptr, A, I32, I32, A, A2, I32, I32, I32, I32, 1 << 20, A2,
+                                       nullptr, nullptr), SPA_ERR_INVALID_ARG);
+  // partials beyond the scratch: refused before any launch
+  reset();
+  spa_dims_t big = dims(1024, 64, 8, 128, 16, 4, 4, 15, 1024 * 15);  // 8192 units x 8 row blocks
+  EXPECT(seg_paged_attn_workspace_size(&big, SPA_SEL_ALL) > SPA_NOALLOC_SCRATCH_BYTES);
+  EXPECT_ST(call(big), SPA_ERR_WORKSPACE);
+  EXPECT(stub::launches.empty());
+  // the largest decode shape that fits runs; chunked prefill keeps no partials
+  spa_dims_t fit = dims(376, 32, 8, 128, 16, 4, 4, 1, 376);           // 3008 units x 1 row block
+  EXPECT(seg_paged_attn_workspace_size(&fit, SPA_SEL_ALL) <= SPA_NOALLOC_SCRATCH_BYTES);
+  EXPECT_ST(call(fit), SPA_OK);
+  EXPECT(launched({"decode_attn", "combine"}));
+  reset();
+  spa_dims_t pre = dims(1024, 64, 8, 128, 16, 4, 4, 512, 1024 * 512);
+  EXPECT_ST(call(pre), SPA_OK);
+  EXPECT(launched({"prefill_attn"}));
+}
+
 int main() {
+  noalloc_paths();
   check_dims_paths();
   select_paths();
   fwd_paths();

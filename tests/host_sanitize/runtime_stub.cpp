@@ -14,6 +14,9 @@ std::vector<std::string> launches;
 hipError_t launch_result = hipSuccess;
 bool validate_reports_bad = false;
 int cus = 256;
+bool symbol_lookup_fails = false;
+int symbol_lookups = 0;
+const float* last_part_o = nullptr;
 
 // Reads every field a launcher hands to a kernel, so a value built from
 // uninitialised or out-of-range host data is touched (and caught) here.
@@ -71,12 +74,30 @@ hipError_t hipMemcpyAsync(void* dst, const void* src, size_t n, hipMemcpyKind, h
   return hipSuccess;
 }
 hipError_t hipStreamSynchronize(hipStream_t) { return hipSuccess; }
+// the scratch's "device address" is its host-side stand-in here (never dereferenced)
+hipError_t hipGetSymbolAddress(void** p, const void* symbol) {
+  ++stub::symbol_lookups;
+  if (p == nullptr || symbol == nullptr) return hipErrorInvalidValue;
+  if (stub::symbol_lookups == 1 && stub::symbol_lookup_fails) return hipErrorInvalidSymbol;
+  *p = const_cast<void*>(symbol);
+  return hipSuccess;
+}
+
+// code-object registration of the library's device variables (nothing to load here)
+static void* g_module = nullptr;
+void** __hipRegisterFatBinary(const void*) { return &g_module; }
+void __hipUnregisterFatBinary(void**) {}
+void __hipRegisterVar(void**, void*, char*, char*, int, size_t, int, int) {}
+// the embedded code-object bundle the host code refers to (its name comes from
+// the compilation unit id and is passed in by the build)
+unsigned char SEGPA_FATBIN_SYMBOL[16] = {0};
 }
 
 // ---- kernel launchers ------------------------------------------------------------
 namespace segpa {
 hipError_t launch_decode(const FwdArgs& a, hipStream_t) {
   stub::touch(a);
+  stub::last_part_o = a.part_o;
   return stub::record("decode_attn");
 }
 hipError_t launch_combine(const FwdArgs& a, hipStream_t) {

@@ -9,7 +9,7 @@ of every entry point (tests/host_sanitize/abi_errors.cpp). Any sanitizer
 report aborts the program; the test needs exit status 0 and no report.
 """
 import os
-import shutil
+import re
 import subprocess
 
 import pytest
@@ -38,12 +38,20 @@ def sanitized_program(tmp_path_factory):
         pytest.fail("hipcc / clang++ of ROCm not found")
     out = tmp_path_factory.mktemp("host_sanitize")
     objs = []
+    defs = []
     for src in (os.path.join(CSRC, "api.cpp"), os.path.join(HERE, "runtime_stub.cpp"),
                 os.path.join(HERE, "abi_errors.cpp")):
         o = str(out / (os.path.splitext(os.path.basename(src))[0] + ".o"))
         _run([HIPCC, "-xhip", "--offload-arch=gfx950", "--cuda-host-only", "-O1", "-g",
-              "-std=c++17", *SAN, "-I", INCLUDE, "-I", CSRC, "-I", HERE, "-c", src, "-o", o])
+              "-std=c++17", *SAN, *defs, "-I", INCLUDE, "-I", CSRC, "-I", HERE, "-c", src, "-o", o])
         objs.append(o)
+        if not defs:
+            # api.cpp holds a device variable: its host code refers to the code-object
+            # bundle by a name derived from the compilation unit; the stand-ins define it
+            nm = _run(["/opt/rocm/llvm/bin/llvm-readelf", "-s", o]).stdout
+            names = [m for m in re.findall(r"UND (__hip_fatbin_\w+)", nm)]
+            assert len(set(names)) == 1, nm
+            defs = [f"-DSEGPA_FATBIN_SYMBOL={names[0]}"]
     exe = str(out / "abi_errors")
     # linked without the HIP runtime: every HIP call the host code makes is a stand-in
     _run([CLANG, "-fsanitize=address,undefined", "-o", exe, *objs])
