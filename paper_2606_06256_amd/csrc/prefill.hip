@@ -19,9 +19,11 @@
 // Per wave and step:
 //   S^T[32 keys x 32 rows]  = K_step[32 x D] . Q^T       (D/16 steps, 32x32x16)
 //   O^T[D x 32 rows]       += V_step^T[D x 32] . P^T     (2 x D/32, 32x32x16)
-// In the S^T layout each lane holds 16 keys of one row, so the row max needs
-// one cross-half swap and the running max, the sum and the rescale are
-// lane-local. The probabilities of tokens 8h..8h+7 of a tile must sit in lane
+// In the S^T layout each lane holds 16 keys of one row, so the sum and the
+// rescale are lane-local. The probabilities of a step are taken against a
+// reference max that moves rarely: a step only checks that each lane's 16
+// probabilities sum to at most 2^8, and only when one does not is the row max
+// formed (one cross-half swap) and the reference moved to it. The probabilities of tokens 8h..8h+7 of a tile must sit in lane
 // half h to meet V rows in token order. The S^T layout gives lane half h the
 // key rows 4h..4h+3 and 8+4h..8+4h+3 of each 16, so key row i of the K
 // operand holds the token whose index is i with bits 2 and 3 exchanged; the
@@ -151,12 +153,12 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
   const int tpp_log2 = a.tpp_log2;
   const int tpp = 1 << tpp_log2;
   const float c = a.scale_log2;
-  const float grow_thr = 8.f / c;          // max growth (raw score units) that forces a rescale
 
-  // The reference max m moves only when a row's max exceeds it by more than
-  // 2^8 in probability; numerator and sum share the reference, so the result
-  // is unchanged, and probabilities stay <= 256, far inside bf16/fp32. The
-  // start value is finite and below any score: the first visible key moves it.
+  // The reference max m moves only when a row's probabilities relative to it
+  // could exceed 2^8 (then it moves to the row max); numerator and sum share
+  // the reference, so the result is unchanged, and probabilities stay <= 256,
+  // far inside bf16/fp32. The start value is finite and below any score: the
+  // first visible key moves it.
   float m = -1e30f;
   float mc = m * c;
   float lsum = 0.f;
@@ -296,20 +298,6 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
           if (!(tp >= 0 && tp + swap_bits23(kk & 15) <= vis_row)) sv[rr] = -INFINITY;
         }
       }
-      float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
-#pragma unroll
-      for (int rr = 3; rr < 15; rr += 2) mx = fmaxf(fmaxf(mx, sv[rr]), sv[rr + 1]);
-      mx = fmaxf(mx, sv[15]);
-      const float m_new = fmaxf(m, max_halves(mx));
-      if (__ballot(m_new - m > grow_thr) != 0ull) {
-        const float mt = m_new - m > grow_thr ? m_new : m;
-        const float alpha = fast_exp2((m - mt) * c);
-        lsum *= alpha;
-#pragma unroll
-        for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
-        m = mt;
-        mc = m * c;
-      }
       return true;
     };
     // exponentials of step st (into pb), interleaved with the scores of step st + 1
@@ -331,12 +319,36 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       }
       nxt = sn_acc;
       __builtin_amdgcn_s_setprio(0);
-      {
+      auto lane_sum = [&]() {
         float t8[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) t8[i] = pv[i] + pv[i + 8];
-        lsum += ((t8[0] + t8[4]) + (t8[1] + t8[5])) + ((t8[2] + t8[6]) + (t8[3] + t8[7]));
+        return ((t8[0] + t8[4]) + (t8[1] + t8[5])) + ((t8[2] + t8[6]) + (t8[3] + t8[7]));
+      };
+      float ps = lane_sum();
+      // A lane's 16 probabilities sum to at most 2^8 unless some score exceeds
+      // the reference max m by more than 8 / c (raw units); only then is the
+      // row max needed. The reference then moves to the row max, everything
+      // accumulated so far is rescaled, and this step's probabilities are
+      // recomputed. (Not "ps <= 256" also catches the first step, where the
+      // reference still holds its start value and the probabilities overflow.)
+      if (__ballot(!(ps <= 256.f)) != 0ull) {
+        float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
+#pragma unroll
+        for (int rr = 3; rr < 15; rr += 2) mx = fmaxf(fmaxf(mx, sv[rr]), sv[rr + 1]);
+        mx = fmaxf(mx, sv[15]);
+        const float m_new = fmaxf(m, max_halves(mx));
+        const float alpha = fast_exp2((m - m_new) * c);
+        lsum *= alpha;
+#pragma unroll
+        for (int d = 0; d < NDB; ++d) acc[d] *= alpha;
+        m = m_new;
+        mc = m * c;
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) pv[rr] = fast_exp2(fmaf(sv[rr], c, -mc));
+        ps = lane_sum();
       }
+      lsum += ps;
       // tile t: pv[8 t .. 8 t + 7] are tokens 8 hf + 0..7, in order
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -348,28 +360,34 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
     // O^T += V^T . P^T for step x: k-slot 8 hf + e of tile t is token 8 hf + e
     // (the matrix-core sections of a wave run at raised issue priority, so
     // that the SIMD's other wave fills their gaps rather than delaying them)
+    // The first four V operands of a step are read ahead (non-lagging waves:
+    // before their score products; lagging waves: at the end of the step
+    // before), so the P.V section does not start on an LDS round trip.
+    constexpr int kVPre = 4;               // <= 2 * NDB for D >= 64
+    s16x8 vpre[kVPre];
+    auto v_operand = [&](int x, int t, int d) -> s16x8 {
+      const char* vb = stage(x) + 2 * TB;
+      const int dd = d * 32 + j;
+      return *reinterpret_cast<const s16x8*>(vb + t * TB + dd * kTile * 2 +
+                                             (hf ^ ((dd >> 3) & 1)) * 16);
+    };
+    auto pv_reads = [&](int x) {
+#pragma unroll
+      for (int i = 0; i < kVPre; ++i) vpre[i] = v_operand(x, i / NDB, i % NDB);
+    };
     auto pv_step = [&](int x, const s16x8 (&pb)[2]) {
       __builtin_amdgcn_s_setprio(1);
-      const char* vb = stage(x) + 2 * TB;
+      s16x8 vrest[2 * NDB - kVPre > 0 ? 2 * NDB - kVPre : 1];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int i = kVPre; i < 2 * NDB; ++i) vrest[i - kVPre] = v_operand(x, i / NDB, i % NDB);
 #pragma unroll
-        for (int d = 0; d < NDB; ++d) {
-          const int dd = d * 32 + j;
-          const s16x8 vop = *reinterpret_cast<const s16x8*>(
-              vb + t * TB + dd * kTile * 2 + (hf ^ ((dd >> 3) & 1)) * 16);
-          acc[d] = mfma32x32x16(vop, pb[t], acc[d]);
-        }
+      for (int i = 0; i < 2 * NDB; ++i) {
+        const s16x8 vop = i < kVPre ? vpre[i] : vrest[i - kVPre];
+        acc[i % NDB] = mfma32x32x16(vop, pb[i / NDB], acc[i % NDB]);
       }
-      // operand reads run four products ahead: 4 reads, then (product, read)
-      // pairs, then the last 4 products
-      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-      for (int i = 0; i < 2 * NDB - 4; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x8, 4, 0);
+      // the remaining operand reads first, then the products
+      if constexpr (2 * NDB > kVPre) __builtin_amdgcn_sched_group_barrier(0x100, 2 * NDB - kVPre, 0);
+      __builtin_amdgcn_sched_group_barrier(0x8, 2 * NDB, 0);
       __builtin_amdgcn_s_setprio(0);
     };
 
@@ -388,6 +406,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       if (st > 0 && (st & 31) == 0) build_table(st);
       if (!lag) {
         if (!pre(st, cur)) return false;
+        pv_reads(st);
         qk_exp(st, cur, nxt, pb);
         pv_step(st, pb);
         fix_partial(st + 2);
@@ -396,6 +415,7 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
         fix_partial(st + 2);
         if (!pre(st, cur)) return false;
         qk_exp(st, cur, nxt, pb);
+        pv_reads(st);
       }
       step_barrier<2 * (kPfAhead - 2)>();
       return true;
