@@ -184,6 +184,10 @@ spa_status_t seg_paged_attn_select(const spa_dims_t* dims, const spa_select_para
  * Shapes: max_q_len * G < 128 runs the split-KV decode kernel (the query rows
  * of a unit in blocks of 16, one matrix-core tile each); larger chunks run the
  * chunked-prefill kernel.
+ * Debug: with the environment variable SEGPA_VALIDATE set (and not "0"), the
+ * call first runs the checks of seg_paged_attn_validate synchronously (so it
+ * then synchronises the stream and cannot be captured in a graph) and returns
+ * SPA_ERR_BAD_DATA without launching when the tables or lists are invalid.
  */
 spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int32_t* q_indptr,
                                 const int32_t* ctx_lens, const void* k_pool, const void* v_pool,

@@ -158,6 +158,16 @@ size_t select_workspace(const spa_dims_t* d, int32_t mode) {
 
 spa_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPA_OK : SPA_ERR_HIP; }
 
+// Debug switch: with SEGPA_VALIDATE set (and not "0") in the environment, the
+// forward calls first run the synchronous table and list check of
+// seg_paged_attn_validate (in the call's workspace) and return its
+// SPA_ERR_BAD_DATA instead of launching. Read on every call (a getenv), so a
+// process can switch it.
+bool validate_switch_on() {
+  const char* s = std::getenv("SEGPA_VALIDATE");
+  return s != nullptr && s[0] != '\0' && !(s[0] == '0' && s[1] == '\0');
+}
+
 // Device address of the current GPU's scratch, looked up on the first call on
 // that device (with it current) and kept per device.
 constexpr int kMaxDevices = 64;
@@ -282,6 +292,12 @@ spa_status_t seg_paged_attn_fwd(const spa_dims_t* dims, const void* q, const int
   if (workspace == nullptr || workspace_bytes < need) return SPA_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) & 15) return SPA_ERR_INVALID_ARG;
   if (dims->total_q == 0) return SPA_OK;
+  if (validate_switch_on()) {
+    st = seg_paged_attn_validate(dims, ctx_lens, q_indptr, seg_table, page_table, sel_indptr,
+                                 sel_pages, sel_capacity, nullptr, nullptr, workspace,
+                                 workspace_bytes, stream);
+    if (st != SPA_OK) return st;
+  }
 
   const int units = (int)units_of(dims);
   FwdArgs a{};

@@ -556,7 +556,33 @@ static void noalloc_paths() {
   EXPECT(launched({"prefill_attn"}));
 }
 
+static void validate_switch_paths() {
+  spa_dims_t d = dims();
+  const size_t ws = seg_paged_attn_workspace_size(&d, SPA_SEL_ALL);
+  Buf wsb(ws + 64);
+  auto fwd = [&]() {
+    return seg_paged_attn_fwd(&d, A, I32, I32, A, A2, I32, I32, I32, I32, 1 << 20, A2, nullptr,
+                              wsb.at(), ws, nullptr);
+  };
+  reset();
+  setenv("SEGPA_VALIDATE", "1", 1);
+  EXPECT_ST(fwd(), SPA_OK);                   // lists found valid: checked, then launched
+  EXPECT(launched({"validate", "decode_attn", "combine"}));
+  reset();
+  stub::validate_reports_bad = true;
+  EXPECT_ST(fwd(), SPA_ERR_BAD_DATA);         // bad lists: nothing launched after the check
+  EXPECT(launched({"validate"}));
+  reset();
+  setenv("SEGPA_VALIDATE", "0", 1);
+  stub::validate_reports_bad = true;
+  EXPECT_ST(fwd(), SPA_OK);                   // switched off: no check
+  EXPECT(launched({"decode_attn", "combine"}));
+  unsetenv("SEGPA_VALIDATE");
+  reset();
+}
+
 int main() {
+  validate_switch_paths();
   noalloc_paths();
   check_dims_paths();
   select_paths();

@@ -420,6 +420,38 @@ def test_validate_reports_bad_lists():
     assert st == -6 and code == 3
 
 
+def test_validate_switch_stops_fwd_on_bad_lists(monkeypatch):
+    """With SEGPA_VALIDATE set, fwd runs the list check first and refuses bad
+    data (SPA_ERR_BAD_DATA, nothing launched); good data gives the ordinary
+    result; unset, the bad page is skipped as usual."""
+    _require_gpu()
+    from paper_2606_06256_amd import binding as B
+    wl = I.build(_spec(name="validate_switch", sel_mode=I.SEL_RANDOM_HASH, budgets=[10, 5],
+                       sel_seed=9))
+    dw = DeviceWorkload(wl)
+    dw.select()
+    dw.fwd()
+    torch.cuda.synchronize()
+    want = dw.out.clone()
+    monkeypatch.setenv("SEGPA_VALIDATE", "1")
+    dw.out.zero_()
+    dw.fwd()                                    # good lists: checked, then the same result
+    torch.cuda.synchronize()
+    assert torch.equal(dw.out, want)
+    good = dw.sel_pages.clone()
+    dw.sel_pages[3] = int(wl.n_pages[0]) + 5    # page id past the context
+    dw.out.fill_(3.0)
+    with pytest.raises(B.SegpaError) as e:
+        dw.fwd()
+    assert e.value.status == -6
+    torch.cuda.synchronize()
+    assert bool((dw.out == 3.0).all())          # nothing was launched
+    monkeypatch.setenv("SEGPA_VALIDATE", "0")
+    dw.fwd()                                    # switch off: the bad page is skipped
+    torch.cuda.synchronize()
+    dw.sel_pages.copy_(good)
+
+
 # --------------------------------------------------------------------------
 # full-size workloads in the benchmark's launch configuration
 # --------------------------------------------------------------------------
