@@ -44,9 +44,11 @@ EXTRA = {"decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
          "prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"]}
 
 
-def _compile(src: str) -> str:
-    out = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *common_flags(), *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", out]
+def _compile(src: str, flags: list[str] = ()) -> str:
+    sub = "poison" if flags else ""
+    out = os.path.join(BUILD, sub, os.path.splitext(src)[0] + ".o")
+    cmd = [hipcc(), *common_flags(), *EXTRA.get(src, []), *flags, "-c", os.path.join(CSRC, src),
+           "-o", out]
     if src.endswith(".cpp"):
         cmd.insert(1, "-xhip")
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -55,18 +57,38 @@ def _compile(src: str) -> str:
     return out
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+# Debug build of the same sources: key and value slots in LDS are filled with
+# NaN before their copies (the kernels that stage tiles through LDS), so a
+# read that is not ordered after its copy corrupts the result visibly.
+POISON_LIB = os.path.join(HERE, "libsegpa_poison.so")
+POISON_FLAGS = ["-DSEGPA_LDS_POISON"]
+
+
+def _link(objs: list[str], lib: str) -> None:
+    tmp = lib + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False, poison: bool = True) -> str:
+    """Builds libsegpa.so and (poison=True) the LDS-poison debug library."""
+    os.makedirs(BUILD, exist_ok=True)
+    jobs = [(s, []) for s in SOURCES]
+    if poison:
+        os.makedirs(os.path.join(BUILD, "poison"), exist_ok=True)
+        jobs += [(s, POISON_FLAGS) for s in SOURCES]
+    with cf.ThreadPoolExecutor(max_workers=8) as ex:
+        objs = list(ex.map(lambda j: _compile(*j), jobs))
+    _link(objs[:len(SOURCES)], LIB)
     if verbose:
         print("built", LIB)
+    if poison:
+        _link(objs[len(SOURCES):], POISON_LIB)
+        if verbose:
+            print("built", POISON_LIB)
     return LIB
 
 

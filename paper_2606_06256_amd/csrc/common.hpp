@@ -112,6 +112,10 @@ __device__ __forceinline__ void copy_to_lds_at(const void* base, int bytes, uint
                :: "s"(m0v), "v"(voff), "s"(rs) : "m0");
 }
 
+// bf16 quiet NaN x 8: what the LDS-poison debug build writes into key and
+// value slots before their copies
+constexpr s16x8 kLdsPoison8 = {0x7FC0, 0x7FC0, 0x7FC0, 0x7FC0, 0x7FC0, 0x7FC0, 0x7FC0, 0x7FC0};
+
 // LDS byte address of a pointer into LDS
 __device__ __forceinline__ uint32_t lds_address(const void* lds) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds;

@@ -143,6 +143,13 @@ __global__ __launch_bounds__(kMassThreads, 1) void token_mass_kernel(const MassA
   int t = tile_of(0);
   if (t - t_lo < n_t) load_rows(t, qa, l_cur);
 
+#ifdef SEGPA_LDS_POISON
+  // debug build: every key slot first holds NaN, so a read of a slot that no
+  // copy filled, or one not ordered after its copy, shows up in the masses
+  for (int i = tid * 16; i < (int)sizeof(s_k); i += kMassThreads * 16)
+    *reinterpret_cast<s16x8*>(s_k + i) = kLdsPoison8;
+  __syncthreads();
+#endif
   // the block's keys into LDS, in pool order (tile m = pool tile tile0 + m);
   // tiles that are not attended are not copied (their columns are dropped)
   for (int x = w; x < nt * PARTS; x += kMassWaves) {

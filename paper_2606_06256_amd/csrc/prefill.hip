@@ -247,6 +247,16 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_kernel(const FwdArgs a)
       const int64_t tile = ent >= 8 ? (int64_t)(ent >> 3) - 1 : 0;
       const int range = ent >= 8 ? TB : 0;
       const uint32_t dst = kv_lds + (uint32_t)((x & (kPfStages - 1)) * SB) + my_lds;
+#ifdef SEGPA_LDS_POISON
+      // debug build: the slots this copy fills first hold NaN, so a read that
+      // is not ordered after the copy's wait and barrier shows up in the output
+      if (range > 0) {
+        char* sl = stage(x) + ct * TB + part * 1024 + lane * 16;
+        *reinterpret_cast<s16x8*>(sl) = kLdsPoison8;
+        *reinterpret_cast<s16x8*>(sl + 2 * TB) = kLdsPoison8;
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      }
+#endif
       copy_to_lds_at(a.k_pool + tile * (kTile * D), range, dst, k_off);
       copy_to_lds_at(a.v_pool + tile * (kTile * D), range, dst + 2 * TB, v_off);
     };
