@@ -143,7 +143,8 @@ def write_traffic_entry(args):
         "hbm_bytes_per_launch": int(read_b + write_b),
         "sources_sha256": kernel_sources_sha256(args.kernel),
         "command": pmc_command(OP_OF_KERNEL.get(args.kernel, "")
-                               + f"--steps 5 --warmup 2 --no-cpu-baseline --workload {args.workload}"),
+                               + f"--steps 5 --warmup 2 --no-cpu-baseline --no-sub-records "
+                               f"--workload {args.workload}"),
     }
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as f:
