@@ -498,7 +498,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=None,
-                    help="named workload 1..9 (default 3, the varlen sparse decode; 9 for --op token_mass)")
+                    help="named workload 1..10 (default 3, the varlen sparse decode; 9 for --op token_mass)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sub-records", default="2,4,5",
                     help="workloads also measured in the same run (step time, dominant-kernel "

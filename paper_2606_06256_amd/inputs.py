@@ -360,8 +360,9 @@ def build(spec: Spec) -> Workload:
 # the five named workloads
 # --------------------------------------------------------------------------
 def config_spec(i: int) -> Spec:
-    """Named workloads 1..9 (shapes of the paper's Llama/Qwen-style layers;
-    6..9 are the head-class micro-benchmark shape of Section 5.3)."""
+    """Named workloads 1..10 (shapes of the paper's Llama/Qwen-style layers;
+    6..9 are the head-class micro-benchmark shape of Section 5.3; 10 is
+    workload 2 as multi-head attention)."""
     seed = 1000 + i
     if i == 1:
         return Spec(name="tiny", B=1, Hq=4, Hkv=4, D=64, P=16, seg_tokens=256,
@@ -405,6 +406,15 @@ def config_spec(i: int) -> Spec:
                     "shifted by +3 along a seeded direction")
     if i in (6, 7, 8):
         return headclass_spec(i, {6: 8192, 7: 32768, 8: 131072}[i], q_len=1)
+    if i == 10:
+        # workload 2 with one query head per KV head (multi-head attention):
+        # a decode tile then fills one row of the 16-row matrix-core tile
+        n = 32768 // 16
+        return Spec(name="mha_decode", B=16, Hq=32, Hkv=32, D=128, P=16, seg_tokens=2048,
+                    ctx_lens=[32768] * 16, q_lens=[1] * 16, seed=seed, sel_mode=SEL_RANDOM_HASH,
+                    budgets=[cdiv(n, 4)] * 16, forced_head=2048 // 16, forced_tail=2048 // 16,
+                    sel_seed=0x5E6A1A, description="batch 16, 32/32 heads (MHA), D128, 32K "
+                    "context in 2048-token segments, page 16, 25% of pages incl. first+last segment")
     if i == 9:
         return headclass_spec(i, 32768, q_len=512)
     raise ValueError(f"no workload {i}")

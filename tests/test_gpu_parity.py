@@ -38,7 +38,7 @@ def test_tiny_config_full():
     PU.run_parity(I.config(1), label="tiny")
 
 
-@pytest.mark.parametrize("i,div,batch", [(2, 16, 4), (3, 32, 6), (5, 32, 3)])
+@pytest.mark.parametrize("i,div,batch", [(2, 16, 4), (3, 32, 6), (5, 32, 3), (10, 16, 3)])
 def test_scaled_decode_configs(i, div, batch):
     _require_gpu()
     PU.run_parity(I.build(I.scaled_spec(i, div, batch)))
@@ -455,7 +455,7 @@ def test_validate_switch_stops_fwd_on_bad_lists(monkeypatch):
 # --------------------------------------------------------------------------
 # full-size workloads in the benchmark's launch configuration
 # --------------------------------------------------------------------------
-@pytest.mark.parametrize("i", [2, 3, 4, 5, 6, 7, 8, 9])
+@pytest.mark.parametrize("i", [2, 3, 4, 5, 6, 7, 8, 9, 10])
 def test_full_size_config(i):
     _require_gpu()
     wl = I.config(i)
