@@ -164,7 +164,7 @@ struct TokSelArgs {
 
 constexpr int kDecodeBlock = 256;   // 4 waves
 constexpr int kSelectBlock = 512;
-constexpr int kSelectKeyCache = 4096;  // keys held in LDS by the select kernel
+constexpr int kSelectKeyCache = 8192;  // candidate keys whose high halves the select kernel holds in LDS
 constexpr int kSelectCand = 1024;      // radix-select candidate list in LDS
 
 hipError_t launch_decode(const FwdArgs& a, hipStream_t stream);

@@ -122,7 +122,9 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
   __shared__ int64_t s_red[BS / 64];
   __shared__ int s_scan[BS / 64];
   __shared__ uint32_t s_hist[4096];
-  __shared__ uint64_t s_keys[kSelectKeyCache];
+  // key cache of the candidates [lo, hi): whole keys for up to
+  // kSelectKeyCache / 2 of them, else the high halves of up to kSelectKeyCache
+  __shared__ uint64_t s_kc[kSelectKeyCache / 2];
   __shared__ uint64_t s_ck[kSelectCand], s_ck2[kSelectCand];
   __shared__ int s_ci[kSelectCand], s_ci2[kSelectCand];
   __shared__ int s_digit, s_need, s_count, s_fill, s_tidx;
@@ -182,7 +184,15 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
   };
   const bool take_all = kk >= nn;
   const bool take_none = kk <= 0;
+  // Units of up to kSelectKeyCache / 2 candidates keep whole keys in LDS.
+  // Larger ones, up to kSelectKeyCache, keep the high 32 bits of each key:
+  // they decide every radix pass whose digits lie in the high half, and the
+  // emission except for keys whose high half equals the threshold's; whole
+  // keys are recomputed (or re-read) only for the candidates left in the
+  // threshold's bin and for such ties. Longer units recompute every key.
+  const bool whole = nn <= kSelectKeyCache / 2;
   const bool cached = nn <= kSelectKeyCache;
+  uint32_t* s_khi = reinterpret_cast<uint32_t*>(s_kc);
   uint64_t T = 0;
   int pT = -1;
   if (!take_all && !take_none) {
@@ -194,12 +204,17 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
       __syncthreads();
       for (int i = tid; i < nn; i += BS) {
         const uint64_t k = key_of(lo + i);
-        s_keys[i] = k;
+        if (whole) s_kc[i] = k; else s_khi[i] = (uint32_t)(k >> 32);
         atomicAdd(&s_hist[(uint32_t)(k >> 52)], 1u);
       }
     }
     __syncthreads();
-    auto key_at = [&](int i) -> uint64_t { return cached ? s_keys[i] : key_of(lo + i); };
+    auto key_full = [&](int i) -> uint64_t { return whole ? s_kc[i] : key_of(lo + i); };
+    // a key for a pass whose fixed bits and digit all lie at bit 32 or above:
+    // its high half suffices (the low half may read as zero)
+    auto key_high = [&](int i) -> uint64_t {
+      return whole ? s_kc[i] : cached ? (uint64_t)s_khi[i] << 32 : key_of(lo + i);
+    };
     // Radix passes narrow the candidates (keys that match `prefix` on the bits
     // of `pmask`): the first pass over all keys with a 12-bit digit, the next
     // ones with 8-bit digits, until at most kRankMax candidates remain or the
@@ -211,17 +226,22 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
     int ncand = nn;
     bool listed = false;            // candidates in s_ck/s_ci, else: filter [lo, hi)
     while (ncand > kRankMax && shift > 0) {
-      const int bits = (shift == 64) ? 12 : 8;
+      // a 12-bit first digit, then 8-bit digits; the last one takes the 4
+      // bits that remain (52 = 6 x 8 + 4), so the shift never goes below 0
+      const int bits = (shift == 64) ? 12 : min(8, shift);
       const int nb = 1 << bits;
       const bool prebuilt = cached && shift == 64;
       shift -= bits;
       const int len = listed ? ncand : nn;
+      // every bit this pass reads (the fixed prefix and the digit) is at shift or above
+      const bool high = shift >= 32;
+      auto key_pass = [&](int i) -> uint64_t { return high ? key_high(i) : key_full(i); };
       if (!prebuilt) {
         for (int i = tid; i < nb; i += BS) s_hist[i] = 0u;
         if (tid == 0) s_fill = 0;
         __syncthreads();
         for (int i = tid; i < len; i += BS) {
-          const uint64_t k = listed ? s_ck[i] : key_at(i);
+          const uint64_t k = listed ? s_ck[i] : key_pass(i);
           if (listed || (k & pmask) == prefix)
             atomicAdd(&s_hist[(uint32_t)(k >> shift) & (uint32_t)(nb - 1)], 1u);
         }
@@ -258,10 +278,10 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
         uint64_t* ck = listed ? s_ck2 : s_ck;
         int* ci = listed ? s_ci2 : s_ci;
         for (int i = tid; i < len; i += BS) {
-          const uint64_t k = listed ? s_ck[i] : key_at(i);
+          const uint64_t k = listed ? s_ck[i] : key_pass(i);
           if ((k & pmask) == prefix) {
             const int slot = atomicAdd(&s_fill, 1);
-            ck[slot] = k;
+            ck[slot] = listed ? k : key_full(i);   // the list holds full keys
             ci[slot] = listed ? s_ci[i] : lo + i;
           }
         }
@@ -281,7 +301,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
       int base = 0;
       for (int c0 = 0; c0 < nn; c0 += BS) {
         const int i = c0 + tid;
-        const bool m = i < nn && key_at(i) == prefix;
+        const bool m = i < nn && key_full(i) == prefix;
         int ex, tot;
         block_scan<BS>(m ? 1 : 0, ex, tot, s_scan);
         if (m && base + ex == need - 1) s_tidx = lo + i;
@@ -291,7 +311,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
     } else {
       if (!listed) {
         // the loop did not run: nn <= kRankMax, every key is a candidate
-        for (int i = tid; i < nn; i += BS) { s_ck[i] = key_at(i); s_ci[i] = lo + i; }
+        for (int i = tid; i < nn; i += BS) { s_ck[i] = key_full(i); s_ci[i] = lo + i; }
         __syncthreads();
       }
       // exact rank of each candidate pair (key, page) among the candidates
@@ -334,8 +354,19 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
       if (nonforced) {
         if (take_all) sel[e] = true;
         else if (!take_none) {
-          const uint64_t k = cached ? s_keys[p - lo] : key_of(p);
-          sel[e] = k < T || (k == T && p <= pT);
+          if (whole) {
+            const uint64_t k = s_kc[p - lo];
+            sel[e] = k < T || (k == T && p <= pT);
+          } else {
+            const uint32_t khi = cached ? s_khi[p - lo] : (uint32_t)(key_of(p) >> 32);
+            const uint32_t thi = (uint32_t)(T >> 32);
+            if (khi != thi) {
+              sel[e] = khi < thi;
+            } else {
+              const uint64_t k = key_of(p);
+              sel[e] = k < T || (k == T && p <= pT);
+            }
+          }
         }
       }
       cnt += sel[e] ? 1 : 0;

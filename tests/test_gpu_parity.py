@@ -118,15 +118,53 @@ EDGE = {
                            forced_tail=1, ctx_lens=[3000, 1500], q_lens=[1, 1], sel_seed=9),
     "page128_topk": dict(P=128, seg_tokens=512, sel_mode=I.SEL_TOPK_MEANKEY, budgets=[4, 2],
                          ctx_lens=[1800, 700]),
-    # more candidate pages than the selection kernel keeps in LDS (4096): the
+    # between 4096 and 8192 candidate pages: key high halves held in LDS
+    "topk_4300_pages": dict(sel_mode=I.SEL_TOPK_MEANKEY, D=64, seg_tokens=4096, budgets=[300, 40],
+                            ctx_lens=[4300 * 16 + 5, 900], shift_pages=40, shift_mag=3.0,
+                            forced_tail=2),
+    "random_4500_pages": dict(sel_mode=I.SEL_RANDOM_HASH, D=64, seg_tokens=4096, budgets=[350, 20],
+                              ctx_lens=[4500 * 16 - 3, 700], forced_head=3, forced_tail=2,
+                              sel_seed=31),
+    # more candidate pages than the selection kernel keeps in LDS (8192): the
     # keys are recomputed in every radix pass
-    "topk_uncached": dict(sel_mode=I.SEL_TOPK_MEANKEY, D=64, seg_tokens=4096, budgets=[300, 40],
-                          ctx_lens=[4300 * 16 + 5, 900], shift_pages=40, shift_mag=3.0,
+    "topk_uncached": dict(sel_mode=I.SEL_TOPK_MEANKEY, D=64, seg_tokens=4096, budgets=[500, 40],
+                          ctx_lens=[8300 * 16 + 5, 900], shift_pages=60, shift_mag=3.0,
                           forced_tail=2),
-    "random_uncached": dict(sel_mode=I.SEL_RANDOM_HASH, D=64, seg_tokens=4096, budgets=[350, 20],
-                            ctx_lens=[4500 * 16 - 3, 700], forced_head=3, forced_tail=2,
+    "random_uncached": dict(sel_mode=I.SEL_RANDOM_HASH, D=64, seg_tokens=4096, budgets=[700, 20],
+                            ctx_lens=[8500 * 16 - 3, 700], forced_head=3, forced_tail=2,
                             sel_seed=31),
 }
+
+
+def test_topk_equal_scores_take_the_lowest_pages():
+    """TOPK where every page of a unit scores the same (its key sums zeroed
+    after the summary build): all 64 key bits tie, the radix passes run down
+    to the low half of the keys and the threshold is decided by the page
+    index; the selection must be the oracle's, i.e. the lowest pages. Units
+    with whole keys in LDS (3,000 pages), with their high halves (6,000) and
+    with none (9,000)."""
+    _require_gpu()
+    from oracle import segpa_oracle as O
+    wl = I.build(_spec(name="topk_ties", B=3, sel_mode=I.SEL_TOPK_MEANKEY, D=64, seg_tokens=4096,
+                       ctx_lens=[9000 * 16 - 5, 3000 * 16 + 3, 6000 * 16], q_lens=[1, 1, 1],
+                       budgets=[600, 50, 400], forced_head=2, forced_tail=3))
+    dw = DeviceWorkload(wl)
+    dw.summary()
+    dw.page_ksum.zero_()
+    dw.select()
+    torch.cuda.synchronize()
+    ind, pages = dw.selection()
+    q64 = wl.q("cpu").double().numpy()
+    for u in range(wl.num_units):
+        r, g = divmod(u, wl.Hkv)
+        L, n = int(wl.ctx_lens[r]), int(wl.n_pages[r])
+        valid = np.minimum(wl.P, L - np.arange(n) * wl.P)
+        last = int(wl.q_indptr[r + 1]) - 1
+        want, _ = O.pages_topk_meankey(q64[last, g * wl.G:(g + 1) * wl.G], np.zeros((n, wl.D)), valid,
+                                       int(wl.budgets[r]), wl.spec.forced_head, wl.spec.forced_tail)
+        got = pages[ind[u]:ind[u + 1]].tolist()
+        assert got == list(want), f"unit {u}: {got[:8]} ... vs {list(want)[:8]} ..."
+
 
 
 @pytest.mark.parametrize("name", sorted(EDGE))
