@@ -125,22 +125,41 @@ __device__ __forceinline__ void copy_to_lds(const void* base, int bytes, const v
   copy_to_lds_at(base, bytes, lds_address(lds), voff);
 }
 
+// Inclusive prefix sum of an int over the 64 lanes of a wave with DPP moves
+// (no LDS round trip): running sums within each row of 16 lanes (shifts by 1,
+// 2, 4, 8; lanes whose source lies before the row's start add 0), then lane
+// 15's sum added to rows 1 and 3 and lane 31's to rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 // Block-wide exclusive prefix sum of one value per thread, in thread order,
-// and the block total (shuffle scan in each wave, then the wave totals in
-// wave order: a fixed order of additions). `scratch` holds BS / 64 values.
+// and the block total (a scan in each wave, then the wave totals in wave
+// order: a fixed order of additions). `scratch` holds BS / 64 values. Ints
+// scan each wave with DPP moves (exact in any order); other types with
+// shuffles, keeping the sequential order within the wave and no subtraction.
 template <int BS, typename T>
 __device__ void block_scan(T x, T& ex, T& tot, T* scratch) {
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   T incl = x;
+  if constexpr (__is_same(T, int)) {
+    incl = wave_incl_scan(x);
+  } else {
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const T y = __shfl_up(incl, o);
-    if (lane >= o) incl += y;
+    for (int o = 1; o < 64; o <<= 1) {
+      const T y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
   }
   if (lane == 63) scratch[w] = incl;
   __syncthreads();
-  const T below = __shfl_up(incl, 1);     // in-wave exclusive sum (no subtraction)
   T pre = 0;
   tot = 0;
 #pragma unroll
@@ -149,7 +168,12 @@ __device__ void block_scan(T x, T& ex, T& tot, T* scratch) {
     if (i < w) pre += c;
     tot += c;
   }
-  ex = lane == 0 ? pre : pre + below;
+  if constexpr (__is_same(T, int)) {
+    ex = pre + (incl - x);
+  } else {
+    const T below = __shfl_up(incl, 1);   // in-wave exclusive sum (no subtraction)
+    ex = lane == 0 ? pre : pre + below;
+  }
   __syncthreads();
 }
 

@@ -192,6 +192,7 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
   // threshold's bin and for such ties. Longer units recompute every key.
   const bool whole = nn <= kSelectKeyCache / 2;
   const bool cached = nn <= kSelectKeyCache;
+  constexpr int kU = 4;   // keys per thread handled together in the full passes
   uint32_t* s_khi = reinterpret_cast<uint32_t*>(s_kc);
   uint64_t T = 0;
   int pT = -1;
@@ -202,10 +203,19 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
       for (int i = tid; i < 4096; i += BS) s_hist[i] = 0u;
       if (tid == 0) s_fill = 0;
       __syncthreads();
-      for (int i = tid; i < nn; i += BS) {
-        const uint64_t k = key_of(lo + i);
-        if (whole) s_kc[i] = k; else s_khi[i] = (uint32_t)(k >> 32);
-        atomicAdd(&s_hist[(uint32_t)(k >> 52)], 1u);
+      // kU keys per thread at a time: their hashes (or loads) are independent
+      for (int i0 = tid; i0 < nn; i0 += kU * BS) {
+        uint64_t kv[kU];
+#pragma unroll
+        for (int e = 0; e < kU; ++e) kv[e] = i0 + e * BS < nn ? key_of(lo + i0 + e * BS) : 0;
+#pragma unroll
+        for (int e = 0; e < kU; ++e) {
+          const int i = i0 + e * BS;
+          if (i < nn) {
+            if (whole) s_kc[i] = kv[e]; else s_khi[i] = (uint32_t)(kv[e] >> 32);
+            atomicAdd(&s_hist[(uint32_t)(kv[e] >> 52)], 1u);
+          }
+        }
       }
     }
     __syncthreads();
@@ -240,10 +250,19 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
         for (int i = tid; i < nb; i += BS) s_hist[i] = 0u;
         if (tid == 0) s_fill = 0;
         __syncthreads();
-        for (int i = tid; i < len; i += BS) {
-          const uint64_t k = listed ? s_ck[i] : key_pass(i);
-          if (listed || (k & pmask) == prefix)
-            atomicAdd(&s_hist[(uint32_t)(k >> shift) & (uint32_t)(nb - 1)], 1u);
+        if (listed) {
+          for (int i = tid; i < len; i += BS)
+            atomicAdd(&s_hist[(uint32_t)(s_ck[i] >> shift) & (uint32_t)(nb - 1)], 1u);
+        } else {
+          for (int i0 = tid; i0 < len; i0 += kU * BS) {
+            uint64_t kv[kU];
+#pragma unroll
+            for (int e = 0; e < kU; ++e) kv[e] = i0 + e * BS < len ? key_pass(i0 + e * BS) : 0;
+#pragma unroll
+            for (int e = 0; e < kU; ++e)
+              if (i0 + e * BS < len && (kv[e] & pmask) == prefix)
+                atomicAdd(&s_hist[(uint32_t)(kv[e] >> shift) & (uint32_t)(nb - 1)], 1u);
+          }
         }
         __syncthreads();
       }
@@ -275,14 +294,29 @@ __global__ __launch_bounds__(kSelectBlock) void select_fill_kernel(const SelArgs
       if (newc <= kSelectCand) {
         // unordered compaction of the survivors (order is irrelevant here);
         // straight into the list unless the list itself is being read
-        uint64_t* ck = listed ? s_ck2 : s_ck;
-        int* ci = listed ? s_ci2 : s_ci;
-        for (int i = tid; i < len; i += BS) {
-          const uint64_t k = listed ? s_ck[i] : key_pass(i);
-          if ((k & pmask) == prefix) {
-            const int slot = atomicAdd(&s_fill, 1);
-            ck[slot] = listed ? k : key_full(i);   // the list holds full keys
-            ci[slot] = listed ? s_ci[i] : lo + i;
+        if (listed) {
+          for (int i = tid; i < len; i += BS) {
+            const uint64_t k = s_ck[i];
+            if ((k & pmask) == prefix) {
+              const int slot = atomicAdd(&s_fill, 1);
+              s_ck2[slot] = k;
+              s_ci2[slot] = s_ci[i];
+            }
+          }
+        } else {
+          for (int i0 = tid; i0 < len; i0 += kU * BS) {
+            uint64_t kv[kU];
+#pragma unroll
+            for (int e = 0; e < kU; ++e) kv[e] = i0 + e * BS < len ? key_pass(i0 + e * BS) : 0;
+#pragma unroll
+            for (int e = 0; e < kU; ++e) {
+              const int i = i0 + e * BS;
+              if (i < len && (kv[e] & pmask) == prefix) {
+                const int slot = atomicAdd(&s_fill, 1);
+                s_ck[slot] = key_full(i);          // the list holds full keys
+                s_ci[slot] = lo + i;
+              }
+            }
           }
         }
         __syncthreads();
