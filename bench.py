@@ -182,7 +182,9 @@ def attention_flops(wl, sel_indptr, sel_pages):
 
 def _cpu_worker(args):
     """One process of the CPU baseline: the fp64 oracle (select + attention)
-    over its units, repeated until `seconds` have passed; single-threaded."""
+    over its units, repeated until `seconds` have passed; single-threaded.
+    Also returns each unit's first result (page list, O, LSE), which the
+    parity entry of the bench line compares with the GPU's."""
     cfg, units, seconds = args
     from threadpoolctl import threadpool_limits
 
@@ -198,6 +200,7 @@ def _cpu_worker(args):
             kv[u] = (K.double().numpy(), V.double().numpy())
         tokens = 0
         done = 0
+        first = {}
         t0 = time.perf_counter()
         while time.perf_counter() - t0 < seconds:
             for u in units:
@@ -207,11 +210,13 @@ def _cpu_worker(args):
                                forced_tail=sp.forced_tail, seed=sp.sel_seed,
                                head_policy=wl.head_policy, n_sink=sp.n_sink, window=sp.window,
                                q=q64, kv_of_unit=lambda rr, gg: (K, V), units=[u])[u]
-                O.forward_unit(q64, wl.q_indptr, wl.ctx_lens, wl.Hq, wl.Hkv, wl.P, u, sel, K, V)
+                res = O.forward_unit(q64, wl.q_indptr, wl.ctx_lens, wl.Hq, wl.Hkv, wl.P, u, sel, K, V)
+                if u not in first:
+                    first[u] = ([int(p) for p in sel], res[0], res[1])
                 L = int(wl.ctx_lens[u // wl.Hkv])
                 tokens += int(sum(min(wl.P, L - p * wl.P) for p in sel))
                 done += 1
-        return tokens, time.perf_counter() - t0, done
+        return tokens, time.perf_counter() - t0, done, first
 
 
 def cpu_baseline(cfg, wl, seconds=12.0, max_procs=16):
@@ -232,10 +237,41 @@ def cpu_baseline(cfg, wl, seconds=12.0, max_procs=16):
     tokens = sum(r[0] for r in res)
     wall = max(r[1] for r in res)
     done = sum(r[2] for r in res)
+    first = {u: v for r in res for u, v in r[3].items()}
     return {"value": tokens / wall, "unit": "tokens/s", "cores": len(shares), "kind": "oracle",
             "sample": f"{len(units)} of {U} (request, KV head) units of one step, {done} unit "
                       f"evaluations in {wall:.1f} s by {len(shares)} single-threaded fp64 numpy "
-                      f"processes (host cores available: {cores})"}
+                      f"processes (host cores available: {cores})"}, first
+
+
+def parity_of_sample(wl, first, ind, pages, out, lse):
+    """The GPU's selection and outputs of the last timed step against the
+    oracle's results for the CPU baseline's sampled units."""
+    G = wl.G
+    mism = 0
+    max_abs = 0.0
+    sum_abs = 0.0
+    n_el = 0
+    lse_max = 0.0
+    for u, (sel, Oo, LSE) in first.items():
+        got = [int(p) for p in pages[int(ind[u]):int(ind[u + 1])]]
+        mism += got != sel
+        r, g = divmod(u, wl.Hkv)
+        q0, q1 = int(wl.q_indptr[r]), int(wl.q_indptr[r + 1])
+        if q1 == q0:
+            continue
+        d = np.abs(out[q0:q1, g * G:(g + 1) * G].astype(np.float64) - Oo)
+        max_abs = max(max_abs, float(d.max()))
+        sum_abs += float(d.sum())
+        n_el += d.size
+        a, b = lse[q0:q1, g * G:(g + 1) * G].astype(np.float64), LSE
+        fin = np.isfinite(a) & np.isfinite(b)
+        if fin.any():
+            lse_max = max(lse_max, float(np.abs(a - b)[fin].max()))
+    return {"units": len(first), "selection_mismatches": int(mism), "o_max_abs": max_abs,
+            "o_mean_abs": sum_abs / max(1, n_el), "lse_max_abs": lse_max,
+            "compared": "the last timed step's page lists, O (bf16) and LSE of the sampled "
+                        "units against the fp64 oracle"}
 
 
 def device_copy_gbs(torch, nbytes=1 << 30, reps=5):
@@ -556,7 +592,7 @@ def main():
         return
 
     # CPU baseline first, before anything initialises the GPU
-    cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, wl)
+    cpu, first = (None, None) if args.no_cpu_baseline else cpu_baseline(args.workload, wl)
 
     import torch
     from paper_2606_06256_amd import binding, build_lib
@@ -566,7 +602,9 @@ def main():
         raise RuntimeError("bench.py needs a GPU")
     torch.cuda.set_device(0)
 
-    head = measure_step(wl, args, torch, binding, cold=True, with_copy=True)
+    head = measure_step(wl, args, torch, binding, cold=True, with_copy=True, check=first)
+    if cpu is not None:
+        cpu["parity"] = head.pop("parity")
     subs = []
     if not args.no_sub_records:
         for i in [int(x) for x in args.sub_records.split(",") if x.strip()]:
@@ -602,9 +640,11 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def measure_step(wl, args, torch, binding, *, cold, with_copy):
+def measure_step(wl, args, torch, binding, *, cold, with_copy, check=None):
     """Warm-up, then exactly args.steps timed steps of `wl` (inputs resident in
-    HBM), then the same number of steps with per-kernel dispatch timing."""
+    HBM), then the same number of steps with per-kernel dispatch timing.
+    With `check` (the oracle's results for some units), the timed steps'
+    outputs are compared with it."""
     from paper_2606_06256_amd import inputs as I
     from paper_2606_06256_amd.device import DeviceWorkload
 
@@ -637,6 +677,10 @@ def measure_step(wl, args, torch, binding, *, cold, with_copy):
     stop.record()
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(stop) / args.steps
+    parity = None
+    if check:
+        parity = parity_of_sample(wl, check, *dw.selection(), dw.out.float().cpu().numpy(),
+                                  dw.lse.cpu().numpy())
 
     # per-kernel launch times: HIP events attached to each kernel dispatch on
     # the stream it is launched on (the kernel's own start and end)
@@ -685,8 +729,11 @@ def measure_step(wl, args, torch, binding, *, cold, with_copy):
     if summary_ms is not None:
         config["page_summary_ms"] = round(summary_ms, 4)
     del dw
-    return {"value": round(tokens / (ms_per_step * 1e-3), 1), "unit": "tokens/s",
-            "ms_per_step": round(ms_per_step, 5), "config": config, "roofline": roofline}
+    out = {"value": round(tokens / (ms_per_step * 1e-3), 1), "unit": "tokens/s",
+           "ms_per_step": round(ms_per_step, 5), "config": config, "roofline": roofline}
+    if check:
+        out["parity"] = parity
+    return out
 
 if __name__ == "__main__":
     main()

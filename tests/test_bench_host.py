@@ -9,6 +9,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
+import numpy as np
+
 import bench  # noqa: E402
 
 
@@ -77,7 +79,43 @@ def test_code_text_ignores_comments_only():
 
 def test_cpu_baseline_pool_reports_what_it_used():
     from paper_2606_06256_amd import inputs as I
-    r = bench.cpu_baseline(1, I.config(1), seconds=0.5, max_procs=2)
+    wl = I.config(1)
+    r, first = bench.cpu_baseline(1, wl, seconds=0.5, max_procs=2)
     assert r["kind"] == "oracle" and r["unit"] == "tokens/s"
     assert r["cores"] == 2 and r["value"] > 0
     assert "2 single-threaded" in r["sample"]
+    # every sampled unit's first result comes back for the parity entry
+    assert sorted(first) == list(range(wl.num_units))
+    sel, Oo, LSE = first[0]
+    assert Oo.shape == (1, wl.G, wl.D) and LSE.shape == (1, wl.G)
+
+
+def test_parity_of_sample_counts_what_differs():
+    """The bench's parity entry: zero against the oracle's own results, then
+    one changed page list and one changed output element are seen."""
+    from paper_2606_06256_amd import inputs as I
+    wl = I.config(1)
+    _, first = bench.cpu_baseline(1, wl, seconds=0.2, max_procs=2)
+    G = wl.G
+    out = np.zeros((wl.total_q, wl.Hq, wl.D), np.float32)
+    lse = np.zeros((wl.total_q, wl.Hq), np.float32)
+    lists = []
+    for u in range(wl.num_units):
+        sel, Oo, LSE = first[u]
+        r, g = divmod(u, wl.Hkv)
+        q0, q1 = int(wl.q_indptr[r]), int(wl.q_indptr[r + 1])
+        out[q0:q1, g * G:(g + 1) * G] = Oo
+        lse[q0:q1, g * G:(g + 1) * G] = LSE
+        lists.append(sel)
+    ind = np.concatenate([[0], np.cumsum([len(x) for x in lists])])
+    pages = np.concatenate(lists)
+    p = bench.parity_of_sample(wl, first, ind, pages, out, lse)
+    assert p["units"] == wl.num_units and p["selection_mismatches"] == 0
+    assert p["o_max_abs"] < 1e-6 and p["lse_max_abs"] < 1e-5
+    pages2 = pages.copy()
+    pages2[int(ind[1])] += 1                  # unit 1's first page
+    out2 = out.copy()
+    out2[0, 0, 3] += 0.5
+    p = bench.parity_of_sample(wl, first, ind, pages2, out2, lse)
+    assert p["selection_mismatches"] == 1
+    assert abs(p["o_max_abs"] - 0.5) < 1e-6
