@@ -91,11 +91,6 @@ int decode_waves(int D, int units) {
     std::lock_guard<std::mutex> lk(g_dev_mu);
     g_decode_waves[key] = waves;
   }
-  // tuning override: blocks of 4 waves per compute unit
-  if (const char* s = std::getenv("SEGPA_DECODE_BLOCKS_PER_CU")) {
-    const int v = std::atoi(s);
-    if (v >= 1 && v <= 64) waves = cus * v * (kDecodeBlock / kWave);
-  }
   return waves;
 }
 
