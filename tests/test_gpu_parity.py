@@ -219,6 +219,20 @@ def test_many_units_short_lists():
     PU.run_parity(I.build(sp), label="many_units")
 
 
+def test_max_units_per_call():
+    """The largest unit count one call takes (B * Hkv = 8192): every unit's
+    page list compared bit for bit, the outputs on a sample of units."""
+    _require_gpu()
+    B = 1024
+    rng = np.random.default_rng(11)
+    ctx = rng.integers(1, 160, size=B).tolist()
+    sp = _spec(name="max_units", B=B, Hq=32, Hkv=8, ctx_lens=ctx, q_lens=[1] * B,
+               sel_mode=I.SEL_RANDOM_HASH, budgets=rng.integers(0, 8, size=B).tolist(), sel_seed=5)
+    wl = I.build(sp)
+    assert wl.num_units == 8192
+    PU.run_parity(wl, units=PU.sample_units(wl.num_units, 64), label="max_units")
+
+
 def test_explicit_lists_with_empty_units():
     _require_gpu()
     wl = I.build(_spec(name="explicit", B=3, ctx_lens=[900, 40, 300], q_lens=[2, 1, 1]))
