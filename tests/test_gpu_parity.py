@@ -103,6 +103,11 @@ EDGE = {
     "prefill_head_class": dict(sel_mode=I.SEL_HEAD_CLASS, head_policy=[0, 1], n_sink=8, window=64,
                                q_lens=[40, 40], ctx_lens=[900, 300]),
     "prefill_rows_g16": dict(Hq=32, Hkv=2, q_lens=[33, 17], ctx_lens=[600, 256]),
+    # either side of the switch between the two kernels (max_q_len * G = 128)
+    "decode_rows_124": dict(q_lens=[31, 20], ctx_lens=[700, 333]),
+    "prefill_rows_128": dict(q_lens=[32, 5], ctx_lens=[700, 333]),
+    "decode_rows_112_g16": dict(Hq=32, Hkv=2, q_lens=[7, 3], ctx_lens=[500, 90]),
+    "prefill_rows_128_g16": dict(Hq=32, Hkv=2, q_lens=[8, 8], ctx_lens=[500, 90]),
     "prefill_many_entries": dict(ctx_lens=[20000, 3000], q_lens=[40, 8], seg_tokens=4096),
     # per-page key scales (LogNormal): scores far apart within a row, so the
     # prefill's running reference max moves several times mid-stream
