@@ -591,8 +591,14 @@ def main():
         bench_token_mass(args, wl)
         return
 
-    # CPU baseline first, before anything initialises the GPU
-    cpu, first = (None, None) if args.no_cpu_baseline else cpu_baseline(args.workload, wl)
+    # CPU baseline first, before anything initialises the GPU (a failure there
+    # is reported in the line rather than losing the GPU measurement)
+    cpu, first = None, None
+    if not args.no_cpu_baseline:
+        try:
+            cpu, first = cpu_baseline(args.workload, wl)
+        except Exception as e:  # noqa: BLE001
+            cpu = {"kind": "oracle", "error": f"{type(e).__name__}: {e}"}
 
     import torch
     from paper_2606_06256_amd import binding, build_lib
@@ -603,7 +609,7 @@ def main():
     torch.cuda.set_device(0)
 
     head = measure_step(wl, args, torch, binding, cold=True, with_copy=True, check=first)
-    if cpu is not None:
+    if cpu is not None and first:
         cpu["parity"] = head.pop("parity")
     subs = []
     if not args.no_sub_records:
@@ -611,7 +617,11 @@ def main():
             if i == args.workload:
                 continue
             torch.cuda.empty_cache()
-            r = measure_step(I.config(i), args, torch, binding, cold=False, with_copy=False)
+            try:
+                r = measure_step(I.config(i), args, torch, binding, cold=False, with_copy=False)
+            except Exception as e:  # noqa: BLE001  (the headline stands on its own)
+                subs.append({"workload": I.config_spec(i).name, "error": f"{type(e).__name__}: {e}"})
+                continue
             subs.append({k: r[k] for k in ("ms_per_step", "value", "unit")} |
                         {"workload": r["config"]["workload"], "roofline": r["roofline"],
                          "kernels": r["config"]["kernels"],
